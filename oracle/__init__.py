@@ -1,0 +1,29 @@
+"""CPU oracle for prefix-shared beam decode attention -- TEST INFRASTRUCTURE.
+
+This package is the parity reference for the HIP library. It is plain,
+slow and written to be checked by eye against its definitions:
+
+* ``attention.oracle_attn`` -- single-query softmax attention per beam and
+  query head over the beam's fully materialised key/value sequence, read
+  through its block table (the paged KV cache of the paper's serving
+  substrate, Sec. 2.3), in fp32.
+* ``prefix_meta.oracle_prefix_meta`` -- the beams of each request arranged
+  as a radix tree (trie) of shared full-block prefixes, grouped so that beams
+  spawned from the same parent are adjacent while the parents keep their
+  relative order (Sec. 4.2, Dynamic Prefix-Aware Scheduling).
+* ``fp8.e4m3_table`` -- the 256 OCP E4M3FN code values from the bit formula.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package. The product path (the HIP library and
+its Python binding) never imports, links or calls it, and the oracle never
+imports the product package: the two share no code. Inputs come from the
+independent ``tts_synth`` generator.
+
+No part of this oracle is "parity unpinned": every function is checked in
+``tests/test_oracle_*.py`` against brute force, closed forms, a library
+routine or hand-derived golden fixtures.
+"""
+
+from .attention import decode_bf16, oracle_attn, oracle_attn_row  # noqa: F401
+from .fp8 import e4m3_table  # noqa: F401
+from .prefix_meta import oracle_coverage, oracle_prefix_meta  # noqa: F401
