@@ -1,0 +1,208 @@
+/*
+ * tts.h -- C ABI of libtts: decode-step attention for test-time-scaling
+ * beam search over a paged KV cache whose blocks are shared along the beams'
+ * common prefixes.
+ *
+ * Problem (FastTTS, Sec. 3.1 and Sec. 4.2): a verifier-guided search keeps N
+ * reasoning beams per request; every decode step each beam issues one query
+ * token that attends over its own cached keys/values. Beams duplicated from
+ * one parent share that parent's KV blocks, so the beams of a request form a
+ * radix tree (trie) of shared prefixes. Decoding is memory-bandwidth bound
+ * (Sec. 3.2.3), so the library reads every shared block once per group of
+ * beams that shares it instead of once per beam.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Status: every call returns tts_status; TTS_OK (0) on success, a negative
+ *   code otherwise. tts_last_error() returns a thread-local message for the
+ *   last failing call of the calling thread. Nothing throws or exits.
+ * - Ownership: the library never allocates or frees caller buffers. Device
+ *   pointers (q, caches, scales, tables, lengths, out, workspace) are owned
+ *   by the caller and must stay valid until the enqueued work completes.
+ *   A tts_prefix_meta handle owns host arrays and one device buffer; free it
+ *   with tts_prefix_meta_destroy.
+ * - Asynchrony: device calls validate their host-visible arguments, enqueue
+ *   kernels on `stream` and return; kernel faults surface at the caller's
+ *   next synchronisation. Calls keep no global state and are reentrant;
+ *   concurrent calls must use distinct workspaces.
+ * - Layouts (row-major, element strides implied by the shapes):
+ *     q          [num_seqs][Hq][D]                     (F32 or BF16)
+ *     k_cache    [num_blocks][Hkv][block_size][D]      token-major blocks
+ *     v_cache    [num_blocks][Hkv][D][block_size]      dim-major blocks
+ *     k_scale, v_scale [num_blocks] fp32               (FP8 caches only)
+ *     block_tables [num_seqs][max_blocks_per_seq] int32 physical block ids
+ *     seq_lens   [num_seqs] int32
+ *     out        [num_seqs][Hq][D] fp32
+ * - Semantics (Sec. 3.1 generation step): seq_lens[b] counts the cached
+ *   tokens of beam b including the current one (its K/V are already in the
+ *   cache). Query head h uses KV head h / (Hq / Hkv). The result is
+ *   softmax(scale * q K^T) V over the beam's seq_lens[b] tokens; a beam with
+ *   seq_len 0 gets a zero row. Table entries at or past
+ *   ceil(seq_len / block_size) are never read, and neither are the unused
+ *   slots of a partially filled last block.
+ * - FP8 KV: OCP E4M3FN codes; the value of a code in block p is
+ *   decode(code) * k_scale[p] (keys) or * v_scale[p] (values).
+ * - Device-side errors: a block id outside [0, num_blocks), a sequence
+ *   longer than its table row, or (prefix call) a beam shorter than the
+ *   metadata was built for makes that beam's output row NaN; no memory
+ *   outside the given buffers is touched.
+ */
+#ifndef TTS_H_
+#define TTS_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TTS_OK = 0,
+  TTS_ERR_INVALID_ARG = -1,
+  TTS_ERR_UNSUPPORTED = -2,
+  TTS_ERR_OUT_OF_RANGE = -3,
+  TTS_ERR_WORKSPACE = -4,
+  TTS_ERR_HIP = -5,
+  TTS_ERR_NOMEM = -6
+} tts_status;
+
+typedef enum { TTS_F32 = 0, TTS_BF16 = 1, TTS_FP8_E4M3 = 2 } tts_dtype;
+
+/* Attention shape. Supported: Hq % Hkv == 0, head_dim 64 or 128,
+ * block_size 16; (q, kv) dtypes (F32, F32), (BF16, BF16), (BF16, FP8_E4M3);
+ * out_dtype F32. scale <= 0 selects 1/sqrt(head_dim). */
+typedef struct {
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t block_size;
+  tts_dtype q_dtype;
+  tts_dtype kv_dtype;
+  tts_dtype out_dtype;
+  float scale;
+} tts_attn_desc;
+
+/* Opaque prefix metadata of one batch of requests (host arrays + one device
+ * buffer with the kernels' work list). */
+typedef struct tts_prefix_meta tts_prefix_meta;
+
+/* Canonical view of the metadata (host pointers, valid until destroy).
+ * perm[i]: original index of the beam at position i. Segments are maximal
+ * chains of trie nodes with the same set of >= 2 beams, listed in depth-first
+ * preorder; segment s covers logical blocks [seg_lblock_begin[s],
+ * seg_lblock_begin[s] + seg_nblocks[s]) of the beams at positions
+ * [seg_beam_begin[s], seg_beam_end[s]) of perm; seg_parent[s] is the
+ * enclosing segment or -1. tail_lblock[b] (original index b) is the first
+ * logical block of beam b not covered by a segment. unique_blocks counts
+ * the distinct physical ids in use; unique_tokens sums, over those ids, the
+ * largest number of valid tokens any beam sees in the block. */
+typedef struct {
+  int32_t num_seqs;
+  int32_t num_segs;
+  const int32_t* perm;
+  const int32_t* seg_req;
+  const int32_t* seg_parent;
+  const int32_t* seg_lblock_begin;
+  const int32_t* seg_nblocks;
+  const int32_t* seg_beam_begin;
+  const int32_t* seg_beam_end;
+  const int32_t* tail_lblock;
+  int64_t unique_blocks;
+  int64_t unique_tokens;
+} tts_prefix_meta_view;
+
+/* Build the prefix metadata of a batch (Sec. 4.2: the beams of each request
+ * form a radix tree of shared thinking prefixes; beams spawned from the same
+ * parent are grouped while the parents keep their relative order).
+ *
+ * All array arguments are HOST int32 arrays; they are copied, not retained.
+ *   req_seq_offsets [num_reqs + 1]: CSR offsets of each request's beams,
+ *       offsets[0] == 0, non-decreasing, offsets[num_reqs] == num_seqs.
+ *   block_tables [num_seqs * max_blocks_per_seq], seq_lens [num_seqs].
+ * Per request, a trie is built over each beam's FULL blocks
+ * (seq_len / block_size of them); only blocks whose id and every preceding
+ * id agree are shared; partial last blocks and blocks of different requests
+ * are never shared. Children are ordered by the smallest original beam index
+ * they contain.
+ * desc: if non-NULL, the kernels' work list for this attention shape is
+ *   built and uploaded to a device buffer on `stream` (the handle can then
+ *   be passed to tts_prefix_decode_attn with the same desc); if NULL, only
+ *   the host-side metadata is built (export/coverage only, no device use).
+ * Errors: TTS_ERR_INVALID_ARG (bad offsets, lengths, sizes, NULL pointers),
+ *   TTS_ERR_OUT_OF_RANGE (a block id in use outside [0, num_blocks)),
+ *   TTS_ERR_UNSUPPORTED (desc shape), TTS_ERR_HIP, TTS_ERR_NOMEM. */
+tts_status tts_build_prefix_meta(int32_t num_reqs, const int32_t* req_seq_offsets, int32_t num_seqs,
+                                 const int32_t* block_tables, int32_t max_blocks_per_seq,
+                                 const int32_t* seq_lens, int32_t block_size, int32_t num_blocks,
+                                 const tts_attn_desc* desc, hipStream_t stream, tts_prefix_meta** out);
+
+/* Free a handle (NULL is ignored). The device buffer is released with
+ * hipFree, which waits for work still using it. */
+void tts_prefix_meta_destroy(tts_prefix_meta* m);
+
+/* Fill `view` with host pointers into the handle's canonical arrays. */
+tts_status tts_prefix_meta_export(const tts_prefix_meta* m, tts_prefix_meta_view* view);
+
+/* Indexing export: one row (beam, lblock, pblock, ntok, src) per used
+ * (beam, logical block), beams in original order and each beam's blocks in
+ * merge order (segments root to leaf, then the tail); src is the covering
+ * segment or -1 for tail blocks. seq_lens_host (may be NULL: build-time
+ * lengths) may exceed the build-time lengths (private appends); pblock of
+ * such rows comes from the tables as given at build time. out_rows holds
+ * cap rows of 5 int32; *n_rows receives the number of rows needed.
+ * TTS_ERR_WORKSPACE if cap is too small (n_rows still set). */
+tts_status tts_prefix_meta_coverage(const tts_prefix_meta* m, const int32_t* seq_lens_host, int32_t* out_rows,
+                                    int64_t cap, int64_t* n_rows);
+
+/* Work-list statistics of a handle built with a desc: number of kernel work
+ * units and partial-result slots (for diagnostics and benchmarks). */
+tts_status tts_prefix_meta_stats(const tts_prefix_meta* m, int64_t* num_units, int64_t* num_slots);
+
+/* Workspace bytes needed by tts_paged_decode_attn for these sizes. */
+size_t tts_paged_decode_workspace_size(const tts_attn_desc* d, int32_t num_seqs, int32_t max_seq_len);
+
+/* Decode attention of every beam over its own paged sequence, without
+ * exploiting sharing: every beam reads all of its blocks (the non-sharing
+ * baseline; paged attention of the serving substrate, Sec. 2.3).
+ * max_seq_len: host upper bound on seq_lens (sizes the split of long
+ * sequences); beams longer than it get NaN rows.
+ * num_blocks: size of the block pool (ids outside it give NaN rows).
+ * workspace: device buffer of at least tts_paged_decode_workspace_size
+ * bytes (TTS_ERR_WORKSPACE otherwise); NULL allowed when that size is 0. */
+tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const void* q, const void* k_cache,
+                                 const void* v_cache, const float* k_scale, const float* v_scale,
+                                 const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                                 int32_t max_seq_len, int32_t num_blocks, void* out, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream);
+
+/* Workspace bytes needed by tts_prefix_decode_attn with this metadata. */
+size_t tts_prefix_decode_workspace_size(const tts_attn_desc* d, const tts_prefix_meta* m);
+
+/* Prefix-shared decode attention (Sec. 4.2 prefix sharing applied to the
+ * decode step): each shared segment's KV blocks are read once per group of
+ * beams sharing them and staged in LDS for all of that group's query rows;
+ * each beam's private tail is read by that beam alone; the pieces are
+ * combined by an exact log-sum-exp merge in a fixed order. Same result as
+ * tts_paged_decode_attn up to rounding.
+ * m: built with the same desc shape and with the same block tables, and
+ * still valid: every table entry a segment covers is unchanged and every
+ * seq_len is >= its value at build time (beams only appended privately).
+ * block_tables/seq_lens: device copies of the current tables and lengths.
+ * workspace: at least tts_prefix_decode_workspace_size bytes. */
+tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
+                                  const void* k_cache, const void* v_cache, const float* k_scale,
+                                  const float* v_scale, const int32_t* block_tables, int32_t max_blocks_per_seq,
+                                  const int32_t* seq_lens, int32_t num_blocks, void* out, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream);
+
+/* Thread-local text of the last error ("" if none). */
+const char* tts_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TTS_H_ */

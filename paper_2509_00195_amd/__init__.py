@@ -1,0 +1,24 @@
+"""MI355X-native prefix-shared beam decode attention (FastTTS hot path).
+
+The compute lives in ``libtts.so`` (HIP for gfx950, C ABI in
+``include/tts.h``); ``tts`` is its ctypes binding and ``device`` moves
+synthetic workloads into device memory with PyTorch (allocation and
+streams only).
+"""
+
+from .tts import (  # noqa: F401
+    EXPORTED,
+    TTSError,
+    PrefixMeta,
+    load,
+    make_desc,
+    tts_build_prefix_meta,
+    tts_paged_decode_attn,
+    tts_paged_decode_workspace_size,
+    tts_prefix_decode_attn,
+    tts_prefix_decode_workspace_size,
+    tts_prefix_meta_coverage,
+    tts_prefix_meta_destroy,
+    tts_prefix_meta_export,
+    tts_prefix_meta_stats,
+)

@@ -1,0 +1,61 @@
+"""Build libtts.so (HIP for gfx950) in-tree.
+
+    python -m paper_2509_00195_amd.build          # or __graft_entry__.build()
+
+Every HIP translation unit is compiled with packed-fp32 instruction
+selection disabled (``-target-feature -packed-fp32-ops``).
+"""
+
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+import sys
+import tempfile
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+LIB = os.path.join(PKG, "libtts.so")
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
+DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+
+SOURCES_HIP = ["tts_kernels.hip"]
+SOURCES_HOST = ["tts_meta.cpp", "tts_api.cpp"]
+
+
+def _run(cmd):
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        sys.stderr.write(r.stdout + r.stderr)
+        raise RuntimeError(f"build step failed: {' '.join(cmd)}")
+    return r
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source and link libtts.so; returns its path."""
+    with tempfile.TemporaryDirectory(prefix="tts_build_") as tmp:
+        objs = []
+        for src in SOURCES_HIP:
+            obj = os.path.join(tmp, src + ".o")
+            _run([HIPCC, *COMMON, *DEVICE, "-c", os.path.join(CSRC, src), "-o", obj])
+            objs.append(obj)
+        for src in SOURCES_HOST:
+            obj = os.path.join(tmp, src + ".o")
+            _run([HIPCC, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj])
+            objs.append(obj)
+        out_tmp = os.path.join(tmp, "libtts.so")
+        _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", out_tmp])
+        shutil.copyfile(out_tmp, LIB + ".tmp")
+        os.replace(LIB + ".tmp", LIB)
+    if verbose:
+        print(f"built {LIB}")
+    return LIB
+
+
+if __name__ == "__main__":
+    build(verbose=True)

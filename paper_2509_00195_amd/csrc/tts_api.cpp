@@ -1,0 +1,369 @@
+// C ABI of libtts (include/tts.h): argument validation, metadata handles
+// and kernel launches.
+#include <hip/hip_runtime_api.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/tts.h"
+#include "tts_meta.h"
+#include "tts_work.h"
+
+namespace tts {
+hipError_t launch_attn_units(const AttnParams& p, int num_units, int head_dim, int kv_kind, hipStream_t stream);
+hipError_t launch_merge(const MergeParams& p, int head_dim, hipStream_t stream);
+}  // namespace tts
+
+namespace {
+
+thread_local std::string g_last_error;
+
+tts_status fail(tts_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+tts_status ok() {
+  g_last_error.clear();
+  return TTS_OK;
+}
+
+// Paged path: blocks per split of a long sequence.
+constexpr int32_t kPagedSplitBlocks = 32;
+
+tts_status check_desc(const tts_attn_desc* d) {
+  if (!d) return fail(TTS_ERR_INVALID_ARG, "desc is NULL");
+  if (d->num_q_heads <= 0 || d->num_kv_heads <= 0 || d->num_q_heads % d->num_kv_heads != 0)
+    return fail(TTS_ERR_INVALID_ARG, "num_q_heads must be a positive multiple of num_kv_heads");
+  if (d->num_q_heads / d->num_kv_heads > tts::kRowsPerUnit)
+    return fail(TTS_ERR_UNSUPPORTED, "more than 64 query heads per KV head");
+  if (d->head_dim != 64 && d->head_dim != 128) return fail(TTS_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (d->block_size != 16) return fail(TTS_ERR_UNSUPPORTED, "block_size must be 16");
+  const bool f32 = d->q_dtype == TTS_F32 && d->kv_dtype == TTS_F32;
+  const bool bf = d->q_dtype == TTS_BF16 && (d->kv_dtype == TTS_BF16 || d->kv_dtype == TTS_FP8_E4M3);
+  if (!f32 && !bf) return fail(TTS_ERR_UNSUPPORTED, "unsupported (q_dtype, kv_dtype) combination");
+  if (d->out_dtype != TTS_F32) return fail(TTS_ERR_UNSUPPORTED, "out_dtype must be F32");
+  if (!std::isfinite(d->scale)) return fail(TTS_ERR_INVALID_ARG, "scale is not finite");
+  return TTS_OK;
+}
+
+int kv_kind(const tts_attn_desc* d) { return d->kv_dtype == TTS_F32 ? 0 : (d->kv_dtype == TTS_BF16 ? 1 : 2); }
+int kv_bytes(const tts_attn_desc* d) { return d->kv_dtype == TTS_F32 ? 4 : (d->kv_dtype == TTS_BF16 ? 2 : 1); }
+
+float scale_log2(const tts_attn_desc* d) {
+  const double s = d->scale > 0.f ? d->scale : 1.0 / std::sqrt(static_cast<double>(d->head_dim));
+  return static_cast<float>(s * 1.4426950408889634);
+}
+
+tts_status check_scales(const tts_attn_desc* d, const float* ks, const float* vs) {
+  if (d->kv_dtype == TTS_FP8_E4M3) {
+    if (!ks || !vs) return fail(TTS_ERR_INVALID_ARG, "fp8 KV needs k_scale and v_scale");
+  } else if (ks || vs) {
+    return fail(TTS_ERR_INVALID_ARG, "k_scale/v_scale must be NULL unless kv_dtype is FP8_E4M3");
+  }
+  return TTS_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+}  // namespace
+
+struct tts_prefix_meta {
+  tts::HostMeta host;
+  bool has_plan = false;
+  tts_attn_desc desc{};
+  tts::WorkPlan plan;
+  int32_t num_blocks = 0;
+  // device buffer: perm | tail_lblock | slot_base | seg_blocks | units
+  void* dev = nullptr;
+  size_t off_perm = 0, off_tail = 0, off_slot = 0, off_seg = 0, off_units = 0;
+};
+
+extern "C" {
+
+const char* tts_last_error(void) { return g_last_error.c_str(); }
+
+tts_status tts_build_prefix_meta(int32_t num_reqs, const int32_t* req_seq_offsets, int32_t num_seqs,
+                                 const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                                 int32_t block_size, int32_t num_blocks, const tts_attn_desc* desc,
+                                 hipStream_t stream, tts_prefix_meta** out) {
+  if (!out) return fail(TTS_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (desc) {
+    tts_status s = check_desc(desc);
+    if (s != TTS_OK) return s;
+    if (desc->block_size != block_size) return fail(TTS_ERR_INVALID_ARG, "desc->block_size != block_size");
+  }
+  tts_prefix_meta* m = new (std::nothrow) tts_prefix_meta();
+  if (!m) return fail(TTS_ERR_NOMEM, "out of host memory");
+  tts::MetaInput in;
+  in.num_reqs = num_reqs;
+  in.req_seq_offsets = req_seq_offsets;
+  in.num_seqs = num_seqs;
+  in.block_tables = block_tables;
+  in.max_blocks = max_blocks_per_seq;
+  in.seq_lens = seq_lens;
+  in.block_size = block_size;
+  in.num_blocks = num_blocks;
+  std::string err;
+  int rc;
+  try {
+    rc = tts::build_host_meta(in, &m->host, &err);
+  } catch (const std::bad_alloc&) {
+    delete m;
+    return fail(TTS_ERR_NOMEM, "out of host memory");
+  }
+  if (rc != 0) {
+    delete m;
+    return fail(static_cast<tts_status>(rc), err);
+  }
+  m->num_blocks = num_blocks;
+  if (desc) {
+    m->has_plan = true;
+    m->desc = *desc;
+    try {
+      tts::build_work_plan(m->host, {desc->num_q_heads, desc->num_kv_heads, desc->head_dim, kv_bytes(desc)},
+                           &m->plan);
+    } catch (const std::bad_alloc&) {
+      delete m;
+      return fail(TTS_ERR_NOMEM, "out of host memory");
+    }
+    const size_t S = static_cast<size_t>(num_seqs);
+    m->off_perm = 0;
+    m->off_tail = align256(m->off_perm + S * 4);
+    m->off_slot = align256(m->off_tail + S * 4);
+    m->off_seg = align256(m->off_slot + (S + 1) * 4);
+    m->off_units = align256(m->off_seg + m->plan.seg_blocks.size() * 4);
+    const size_t total = align256(m->off_units + m->plan.units.size() * sizeof(tts::Unit));
+    std::vector<unsigned char> img(total, 0);
+    std::memcpy(img.data() + m->off_perm, m->host.perm.data(), S * 4);
+    std::memcpy(img.data() + m->off_tail, m->host.tail_lblock.data(), S * 4);
+    std::memcpy(img.data() + m->off_slot, m->plan.slot_base.data(), (S + 1) * 4);
+    if (!m->plan.seg_blocks.empty())
+      std::memcpy(img.data() + m->off_seg, m->plan.seg_blocks.data(), m->plan.seg_blocks.size() * 4);
+    if (!m->plan.units.empty())
+      std::memcpy(img.data() + m->off_units, m->plan.units.data(), m->plan.units.size() * sizeof(tts::Unit));
+    hipError_t e = hipMalloc(&m->dev, total);
+    if (e != hipSuccess) {
+      m->dev = nullptr;
+      delete m;
+      return fail(e == hipErrorOutOfMemory ? TTS_ERR_NOMEM : TTS_ERR_HIP,
+                  std::string("hipMalloc: ") + hipGetErrorString(e));
+    }
+    e = hipMemcpyAsync(m->dev, img.data(), total, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);  // img is a temporary host buffer
+    if (e != hipSuccess) {
+      hipFree(m->dev);
+      delete m;
+      return fail(TTS_ERR_HIP, std::string("upload: ") + hipGetErrorString(e));
+    }
+  }
+  *out = m;
+  return ok();
+}
+
+void tts_prefix_meta_destroy(tts_prefix_meta* m) {
+  if (!m) return;
+  if (m->dev) hipFree(m->dev);
+  delete m;
+}
+
+tts_status tts_prefix_meta_export(const tts_prefix_meta* m, tts_prefix_meta_view* v) {
+  if (!m || !v) return fail(TTS_ERR_INVALID_ARG, "NULL argument");
+  const auto& h = m->host;
+  v->num_seqs = h.num_seqs;
+  v->num_segs = static_cast<int32_t>(h.seg_req.size());
+  v->perm = h.perm.data();
+  v->seg_req = h.seg_req.data();
+  v->seg_parent = h.seg_parent.data();
+  v->seg_lblock_begin = h.seg_lblock_begin.data();
+  v->seg_nblocks = h.seg_nblocks.data();
+  v->seg_beam_begin = h.seg_beam_begin.data();
+  v->seg_beam_end = h.seg_beam_end.data();
+  v->tail_lblock = h.tail_lblock.data();
+  v->unique_blocks = h.unique_blocks;
+  v->unique_tokens = h.unique_tokens;
+  return ok();
+}
+
+tts_status tts_prefix_meta_coverage(const tts_prefix_meta* m, const int32_t* seq_lens_host, int32_t* out_rows,
+                                    int64_t cap, int64_t* n_rows) {
+  if (!m || !n_rows) return fail(TTS_ERR_INVALID_ARG, "NULL argument");
+  if (cap < 0 || (cap > 0 && !out_rows)) return fail(TTS_ERR_INVALID_ARG, "bad out_rows/cap");
+  if (seq_lens_host) {
+    for (int32_t b = 0; b < m->host.num_seqs; ++b) {
+      if (seq_lens_host[b] < 0 || static_cast<int64_t>(seq_lens_host[b]) >
+                                      static_cast<int64_t>(m->host.max_blocks) * m->host.block_size)
+        return fail(TTS_ERR_INVALID_ARG, "seq_lens_host entry outside [0, max_blocks * block_size]");
+    }
+  }
+  *n_rows = tts::coverage_rows(m->host, seq_lens_host, out_rows, cap);
+  if (*n_rows > cap) return fail(TTS_ERR_WORKSPACE, "cap too small for the coverage rows");
+  return ok();
+}
+
+tts_status tts_prefix_meta_stats(const tts_prefix_meta* m, int64_t* num_units, int64_t* num_slots) {
+  if (!m || !num_units || !num_slots) return fail(TTS_ERR_INVALID_ARG, "NULL argument");
+  if (!m->has_plan) return fail(TTS_ERR_INVALID_ARG, "metadata was built without a desc");
+  *num_units = static_cast<int64_t>(m->plan.units.size());
+  *num_slots = m->plan.num_slots;
+  return ok();
+}
+
+static int32_t paged_nsplit(int32_t max_seq_len) {
+  const int32_t nblk = (max_seq_len + 15) / 16;
+  const int32_t n = (nblk + kPagedSplitBlocks - 1) / kPagedSplitBlocks;
+  return n < 1 ? 1 : n;
+}
+
+size_t tts_paged_decode_workspace_size(const tts_attn_desc* d, int32_t num_seqs, int32_t max_seq_len) {
+  if (!d || check_desc(d) != TTS_OK || num_seqs < 0 || max_seq_len < 0) return 0;
+  const int32_t ns = paged_nsplit(max_seq_len);
+  if (ns == 1) return 0;
+  const size_t rows = static_cast<size_t>(num_seqs) * ns * d->num_q_heads;
+  return align256(rows * d->head_dim * 4) + align256(rows * 2 * 4);
+}
+
+tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const void* q, const void* k_cache,
+                                 const void* v_cache, const float* k_scale, const float* v_scale,
+                                 const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                                 int32_t max_seq_len, int32_t num_blocks, void* out, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  tts_status s = check_desc(d);
+  if (s != TTS_OK) return s;
+  if ((s = check_scales(d, k_scale, v_scale)) != TTS_OK) return s;
+  if (num_seqs < 0 || max_blocks_per_seq < 0 || max_seq_len < 0 || num_blocks < 0)
+    return fail(TTS_ERR_INVALID_ARG, "negative size");
+  if (static_cast<int64_t>(max_seq_len) > static_cast<int64_t>(max_blocks_per_seq) * 16)
+    return fail(TTS_ERR_INVALID_ARG, "max_seq_len exceeds max_blocks_per_seq * block_size");
+  if (num_seqs == 0) return ok();
+  if (!q || !k_cache || !v_cache || !block_tables || !seq_lens || !out)
+    return fail(TTS_ERR_INVALID_ARG, "NULL device pointer");
+  const int32_t ns = paged_nsplit(max_seq_len);
+  const size_t need = tts_paged_decode_workspace_size(d, num_seqs, max_seq_len);
+  if (need > 0 && (!workspace || workspace_bytes < need))
+    return fail(TTS_ERR_WORKSPACE, "workspace smaller than tts_paged_decode_workspace_size");
+  const size_t rows = static_cast<size_t>(num_seqs) * ns * d->num_q_heads;
+  tts::AttnParams p{};
+  p.q = q;
+  p.k_cache = k_cache;
+  p.v_cache = v_cache;
+  p.k_scale = k_scale;
+  p.v_scale = v_scale;
+  p.block_tables = block_tables;
+  p.seq_lens = seq_lens;
+  p.out = static_cast<float*>(out);
+  p.part_o = ns > 1 ? static_cast<float*>(workspace) : nullptr;
+  p.part_ml = ns > 1 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * d->head_dim * 4))
+                     : nullptr;
+  p.max_blocks = max_blocks_per_seq;
+  p.num_blocks = num_blocks;
+  p.num_seqs = num_seqs;
+  p.hq = d->num_q_heads;
+  p.hkv = d->num_kv_heads;
+  p.g = d->num_q_heads / d->num_kv_heads;
+  p.scale_log2 = scale_log2(d);
+  p.paged_nsplit = ns;
+  p.paged_max_len = max_seq_len;
+  const int64_t units = static_cast<int64_t>(num_seqs) * d->num_kv_heads * ns;
+  if (units > 0x7FFFFFFF) return fail(TTS_ERR_UNSUPPORTED, "grid too large");
+  hipError_t e = tts::launch_attn_units(p, static_cast<int>(units), d->head_dim, kv_kind(d), stream);
+  if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("attention launch: ") + hipGetErrorString(e));
+  if (ns > 1) {
+    tts::MergeParams mp{};
+    mp.part_o = p.part_o;
+    mp.part_ml = p.part_ml;
+    mp.slot_base = nullptr;
+    mp.seq_lens = seq_lens;
+    mp.tail_lblock = nullptr;
+    mp.out = p.out;
+    mp.num_seqs = num_seqs;
+    mp.hq = d->num_q_heads;
+    mp.paged_nsplit = ns;
+    mp.block_size = 16;
+    e = tts::launch_merge(mp, d->head_dim, stream);
+    if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
+  }
+  return ok();
+}
+
+size_t tts_prefix_decode_workspace_size(const tts_attn_desc* d, const tts_prefix_meta* m) {
+  if (!d || !m || !m->has_plan || check_desc(d) != TTS_OK) return 0;
+  const size_t rows = static_cast<size_t>(m->plan.num_slots) * d->num_q_heads;
+  return align256(rows * d->head_dim * 4) + align256(rows * 2 * 4);
+}
+
+tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
+                                  const void* k_cache, const void* v_cache, const float* k_scale,
+                                  const float* v_scale, const int32_t* block_tables, int32_t max_blocks_per_seq,
+                                  const int32_t* seq_lens, int32_t num_blocks, void* out, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  tts_status s = check_desc(d);
+  if (s != TTS_OK) return s;
+  if ((s = check_scales(d, k_scale, v_scale)) != TTS_OK) return s;
+  if (!m) return fail(TTS_ERR_INVALID_ARG, "metadata is NULL");
+  if (!m->has_plan || !m->dev) return fail(TTS_ERR_INVALID_ARG, "metadata was built without a desc");
+  if (m->desc.num_q_heads != d->num_q_heads || m->desc.num_kv_heads != d->num_kv_heads ||
+      m->desc.head_dim != d->head_dim)
+    return fail(TTS_ERR_INVALID_ARG, "desc shape differs from the one the metadata was built for");
+  if (max_blocks_per_seq != m->host.max_blocks)
+    return fail(TTS_ERR_INVALID_ARG, "max_blocks_per_seq differs from the metadata's");
+  if (num_blocks < m->num_blocks) return fail(TTS_ERR_INVALID_ARG, "num_blocks smaller than at build time");
+  const int32_t S = m->host.num_seqs;
+  if (S == 0) return ok();
+  if (!q || !k_cache || !v_cache || !block_tables || !seq_lens || !out)
+    return fail(TTS_ERR_INVALID_ARG, "NULL device pointer");
+  const size_t need = tts_prefix_decode_workspace_size(d, m);
+  if (!workspace || workspace_bytes < need)
+    return fail(TTS_ERR_WORKSPACE, "workspace smaller than tts_prefix_decode_workspace_size");
+  const size_t rows = static_cast<size_t>(m->plan.num_slots) * d->num_q_heads;
+  const char* dev = static_cast<const char*>(m->dev);
+  tts::AttnParams p{};
+  p.q = q;
+  p.k_cache = k_cache;
+  p.v_cache = v_cache;
+  p.k_scale = k_scale;
+  p.v_scale = v_scale;
+  p.block_tables = block_tables;
+  p.seq_lens = seq_lens;
+  p.out = static_cast<float*>(out);
+  p.part_o = static_cast<float*>(workspace);
+  p.part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * d->head_dim * 4));
+  p.perm = reinterpret_cast<const int32_t*>(dev + m->off_perm);
+  p.tail_lblock = reinterpret_cast<const int32_t*>(dev + m->off_tail);
+  p.slot_base = reinterpret_cast<const int32_t*>(dev + m->off_slot);
+  p.seg_blocks = reinterpret_cast<const int32_t*>(dev + m->off_seg);
+  p.units = reinterpret_cast<const tts::Unit*>(dev + m->off_units);
+  p.max_blocks = max_blocks_per_seq;
+  p.num_blocks = num_blocks;
+  p.num_seqs = S;
+  p.hq = d->num_q_heads;
+  p.hkv = d->num_kv_heads;
+  p.g = d->num_q_heads / d->num_kv_heads;
+  p.scale_log2 = scale_log2(d);
+  p.paged_nsplit = 0;
+  p.paged_max_len = 0;
+  hipError_t e =
+      tts::launch_attn_units(p, static_cast<int>(m->plan.units.size()), d->head_dim, kv_kind(d), stream);
+  if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("attention launch: ") + hipGetErrorString(e));
+  tts::MergeParams mp{};
+  mp.part_o = p.part_o;
+  mp.part_ml = p.part_ml;
+  mp.slot_base = p.slot_base;
+  mp.seq_lens = seq_lens;
+  mp.tail_lblock = p.tail_lblock;
+  mp.out = p.out;
+  mp.num_seqs = S;
+  mp.hq = d->num_q_heads;
+  mp.paged_nsplit = 0;
+  mp.block_size = 16;
+  e = tts::launch_merge(mp, d->head_dim, stream);
+  if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

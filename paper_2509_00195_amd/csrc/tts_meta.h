@@ -1,0 +1,73 @@
+// Host-side prefix metadata and kernel work list (pure C++, no HIP).
+//
+// The beams of each request form a radix tree (trie) of shared thinking
+// prefixes (FastTTS Sec. 4.2). Here the trie is built over physical KV block
+// ids: a node is a prefix of full blocks, its beam set the beams whose
+// full-block path starts with it. Maximal chains of nodes with the same set
+// of >= 2 beams are "segments"; each segment's blocks are read once for all
+// of its beams. Beams are ordered depth-first with children sorted by their
+// smallest original beam index, which groups siblings while the parents keep
+// their relative order (Sec. 4.2), and makes each segment's beams a
+// contiguous range of positions.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "tts_work.h"
+
+namespace tts {
+
+struct MetaInput {
+  int32_t num_reqs = 0;
+  const int32_t* req_seq_offsets = nullptr;
+  int32_t num_seqs = 0;
+  const int32_t* block_tables = nullptr;
+  int32_t max_blocks = 0;
+  const int32_t* seq_lens = nullptr;
+  int32_t block_size = 16;
+  int32_t num_blocks = 0;
+};
+
+struct HostMeta {
+  int32_t num_seqs = 0;
+  int32_t block_size = 16;
+  int32_t max_blocks = 0;
+  // canonical arrays
+  std::vector<int32_t> perm;  // position -> original beam
+  std::vector<int32_t> seg_req, seg_parent, seg_lblock_begin, seg_nblocks, seg_beam_begin, seg_beam_end;
+  std::vector<int32_t> tail_lblock;  // by original beam
+  int64_t unique_blocks = 0, unique_tokens = 0;
+  // per beam: covering segment of each logical block below tail_lblock (CSR)
+  std::vector<int32_t> path_seg_off, path_seg;
+  // build-time copies
+  std::vector<int32_t> tables, seq_lens;
+  std::vector<int32_t> pos_of;  // original beam -> position
+};
+
+// Validates the input and builds the canonical metadata. Returns 0 on
+// success or a negative tts_status code with a message in *err.
+int build_host_meta(const MetaInput& in, HostMeta* out, std::string* err);
+
+// Coverage rows (beam, lblock, pblock, ntok, src) for the given lengths
+// (build-time lengths when seq_lens is null). Returns the number of rows;
+// writes at most cap rows.
+int64_t coverage_rows(const HostMeta& m, const int32_t* seq_lens, int32_t* rows, int64_t cap);
+
+// Kernel work list for one attention shape.
+struct WorkPlan {
+  std::vector<Unit> units;
+  std::vector<int32_t> seg_blocks;  // physical ids of every segment piece
+  std::vector<int32_t> slot_base;   // [S + 1] by original beam
+  std::vector<int32_t> tail_nsplit; // by original beam
+  int64_t num_slots = 0;
+};
+
+struct PlanShape {
+  int32_t num_q_heads, num_kv_heads, head_dim, kv_bytes;
+};
+
+void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan);
+
+}  // namespace tts

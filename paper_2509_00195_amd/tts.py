@@ -1,0 +1,249 @@
+"""Python binding of libtts (argument marshalling only).
+
+Every function forwards to the C ABI of ``include/tts.h`` with the same
+name; all computation happens in the HIP library. Device buffers are passed
+as torch tensors (their ``data_ptr()``) or raw integer addresses; host arrays
+as numpy int32 arrays. The library is loaded from this package's directory;
+if it has not been built, loading raises instead of falling back to
+anything else.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtts.so")
+
+TTS_OK = 0
+TTS_ERR_INVALID_ARG = -1
+TTS_ERR_UNSUPPORTED = -2
+TTS_ERR_OUT_OF_RANGE = -3
+TTS_ERR_WORKSPACE = -4
+TTS_ERR_HIP = -5
+TTS_ERR_NOMEM = -6
+STATUS_NAMES = {0: "TTS_OK", -1: "TTS_ERR_INVALID_ARG", -2: "TTS_ERR_UNSUPPORTED", -3: "TTS_ERR_OUT_OF_RANGE",
+                -4: "TTS_ERR_WORKSPACE", -5: "TTS_ERR_HIP", -6: "TTS_ERR_NOMEM"}
+
+TTS_F32, TTS_BF16, TTS_FP8_E4M3 = 0, 1, 2
+DTYPES = {"f32": TTS_F32, "bf16": TTS_BF16, "fp8": TTS_FP8_E4M3}
+
+EXPORTED = [
+    "tts_build_prefix_meta", "tts_prefix_meta_destroy", "tts_prefix_meta_export", "tts_prefix_meta_coverage",
+    "tts_prefix_meta_stats", "tts_paged_decode_workspace_size", "tts_paged_decode_attn",
+    "tts_prefix_decode_workspace_size", "tts_prefix_decode_attn", "tts_last_error",
+]
+
+
+class TTSError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+class tts_attn_desc(C.Structure):
+    _fields_ = [("num_q_heads", C.c_int32), ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("block_size", C.c_int32), ("q_dtype", C.c_int), ("kv_dtype", C.c_int), ("out_dtype", C.c_int),
+                ("scale", C.c_float)]
+
+
+class tts_prefix_meta_view(C.Structure):
+    _fields_ = [("num_seqs", C.c_int32), ("num_segs", C.c_int32), ("perm", C.POINTER(C.c_int32)),
+                ("seg_req", C.POINTER(C.c_int32)), ("seg_parent", C.POINTER(C.c_int32)),
+                ("seg_lblock_begin", C.POINTER(C.c_int32)), ("seg_nblocks", C.POINTER(C.c_int32)),
+                ("seg_beam_begin", C.POINTER(C.c_int32)), ("seg_beam_end", C.POINTER(C.c_int32)),
+                ("tail_lblock", C.POINTER(C.c_int32)), ("unique_blocks", C.c_int64),
+                ("unique_tokens", C.c_int64)]
+
+
+_lib = None
+
+
+def load() -> C.CDLL:
+    """Load libtts.so (raises if it is missing)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} not built: run __graft_entry__.build() or python -m paper_2509_00195_amd.build")
+    lib = C.CDLL(LIB_PATH)
+    P, I32, I64, VP = C.POINTER, C.c_int32, C.c_int64, C.c_void_p
+    pi32 = P(C.c_int32)
+    lib.tts_last_error.restype = C.c_char_p
+    lib.tts_last_error.argtypes = []
+    lib.tts_build_prefix_meta.restype = C.c_int
+    lib.tts_build_prefix_meta.argtypes = [I32, pi32, I32, pi32, I32, pi32, I32, I32, P(tts_attn_desc), VP, P(VP)]
+    lib.tts_prefix_meta_destroy.restype = None
+    lib.tts_prefix_meta_destroy.argtypes = [VP]
+    lib.tts_prefix_meta_export.restype = C.c_int
+    lib.tts_prefix_meta_export.argtypes = [VP, P(tts_prefix_meta_view)]
+    lib.tts_prefix_meta_coverage.restype = C.c_int
+    lib.tts_prefix_meta_coverage.argtypes = [VP, pi32, pi32, I64, P(I64)]
+    lib.tts_prefix_meta_stats.restype = C.c_int
+    lib.tts_prefix_meta_stats.argtypes = [VP, P(I64), P(I64)]
+    lib.tts_paged_decode_workspace_size.restype = C.c_size_t
+    lib.tts_paged_decode_workspace_size.argtypes = [P(tts_attn_desc), I32, I32]
+    lib.tts_paged_decode_attn.restype = C.c_int
+    lib.tts_paged_decode_attn.argtypes = [P(tts_attn_desc), I32, VP, VP, VP, VP, VP, VP, I32, VP, I32, I32, VP, VP,
+                                          C.c_size_t, VP]
+    lib.tts_prefix_decode_workspace_size.restype = C.c_size_t
+    lib.tts_prefix_decode_workspace_size.argtypes = [P(tts_attn_desc), VP]
+    lib.tts_prefix_decode_attn.restype = C.c_int
+    lib.tts_prefix_decode_attn.argtypes = [P(tts_attn_desc), VP, VP, VP, VP, VP, VP, VP, I32, VP, I32, VP, VP,
+                                           C.c_size_t, VP]
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != TTS_OK:
+        raise TTSError(status, load().tts_last_error().decode())
+
+
+def make_desc(num_q_heads, num_kv_heads, head_dim, block_size=16, q_dtype="bf16", kv_dtype="bf16",
+              out_dtype="f32", scale=0.0) -> tts_attn_desc:
+    dt = lambda x: DTYPES[x] if isinstance(x, str) else int(x)  # noqa: E731
+    return tts_attn_desc(num_q_heads, num_kv_heads, head_dim, block_size, dt(q_dtype), dt(kv_dtype), dt(out_dtype),
+                         float(scale))
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        if not x.is_contiguous():
+            raise ValueError("device tensors must be contiguous")
+        return x.data_ptr()
+    raise TypeError(f"cannot pass {type(x)} as a device pointer")
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        try:
+            import torch
+
+            if torch.cuda.is_available():
+                return torch.cuda.current_stream().cuda_stream
+        except Exception:  # pragma: no cover - torch missing
+            pass
+        return None
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _host_i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _as_i32p(a: np.ndarray):
+    return a.ctypes.data_as(C.POINTER(C.c_int32))
+
+
+class PrefixMeta:
+    """Owning wrapper of a ``tts_prefix_meta*`` handle."""
+
+    def __init__(self, handle: int, desc: Optional[tts_attn_desc]):
+        self.handle = handle
+        self.desc = desc
+
+    def __del__(self):
+        self.destroy()
+
+    def destroy(self):
+        if getattr(self, "handle", None):
+            tts_prefix_meta_destroy(self)
+            self.handle = None
+
+    def export(self) -> dict:
+        return tts_prefix_meta_export(self)
+
+    def coverage(self, seq_lens_host=None) -> np.ndarray:
+        return tts_prefix_meta_coverage(self, seq_lens_host)
+
+    def stats(self):
+        return tts_prefix_meta_stats(self)
+
+
+def tts_build_prefix_meta(req_seq_offsets, block_tables, seq_lens, block_size: int, num_blocks: int,
+                          desc: Optional[tts_attn_desc] = None, stream=None) -> PrefixMeta:
+    lib = load()
+    offs = _host_i32(req_seq_offsets)
+    tables = _host_i32(block_tables)
+    lens = _host_i32(seq_lens)
+    s = lens.shape[0]
+    maxb = tables.shape[1] if tables.ndim == 2 else 0
+    h = C.c_void_p()
+    _check(lib.tts_build_prefix_meta(offs.shape[0] - 1, _as_i32p(offs), s, _as_i32p(tables), maxb, _as_i32p(lens),
+                                     block_size, num_blocks, C.byref(desc) if desc is not None else None,
+                                     _stream(stream) if desc is not None else None, C.byref(h)))
+    return PrefixMeta(h.value, desc)
+
+
+def tts_prefix_meta_destroy(meta: PrefixMeta):
+    load().tts_prefix_meta_destroy(meta.handle)
+
+
+def tts_prefix_meta_export(meta: PrefixMeta) -> dict:
+    v = tts_prefix_meta_view()
+    _check(load().tts_prefix_meta_export(meta.handle, C.byref(v)))
+    arr = lambda p, n: np.ctypeslib.as_array(p, shape=(n,)).copy() if n else np.zeros(0, np.int32)  # noqa: E731
+    s, g = v.num_seqs, v.num_segs
+    return {
+        "num_seqs": s, "num_segs": g, "perm": arr(v.perm, s), "seg_req": arr(v.seg_req, g),
+        "seg_parent": arr(v.seg_parent, g), "seg_lblock_begin": arr(v.seg_lblock_begin, g),
+        "seg_nblocks": arr(v.seg_nblocks, g), "seg_beam_begin": arr(v.seg_beam_begin, g),
+        "seg_beam_end": arr(v.seg_beam_end, g), "tail_lblock": arr(v.tail_lblock, s),
+        "unique_blocks": int(v.unique_blocks), "unique_tokens": int(v.unique_tokens),
+    }
+
+
+def tts_prefix_meta_coverage(meta: PrefixMeta, seq_lens_host=None) -> np.ndarray:
+    lib = load()
+    lens = None if seq_lens_host is None else _host_i32(seq_lens_host)
+    lp = _as_i32p(lens) if lens is not None else None
+    n = C.c_int64(0)
+    st = lib.tts_prefix_meta_coverage(meta.handle, lp, None, 0, C.byref(n))
+    if st not in (TTS_OK, TTS_ERR_WORKSPACE):
+        _check(st)
+    rows = np.zeros((max(1, n.value), 5), np.int32)
+    _check(lib.tts_prefix_meta_coverage(meta.handle, lp, _as_i32p(rows), rows.shape[0], C.byref(n)))
+    return rows[: n.value]
+
+
+def tts_prefix_meta_stats(meta: PrefixMeta):
+    u, s = C.c_int64(0), C.c_int64(0)
+    _check(load().tts_prefix_meta_stats(meta.handle, C.byref(u), C.byref(s)))
+    return u.value, s.value
+
+
+def tts_paged_decode_workspace_size(desc: tts_attn_desc, num_seqs: int, max_seq_len: int) -> int:
+    return int(load().tts_paged_decode_workspace_size(C.byref(desc), num_seqs, max_seq_len))
+
+
+def tts_prefix_decode_workspace_size(desc: tts_attn_desc, meta: PrefixMeta) -> int:
+    return int(load().tts_prefix_decode_workspace_size(C.byref(desc), meta.handle))
+
+
+def tts_paged_decode_attn(desc: tts_attn_desc, num_seqs: int, q, k_cache, v_cache, k_scale, v_scale, block_tables,
+                          max_blocks_per_seq: int, seq_lens, max_seq_len: int, num_blocks: int, out, workspace,
+                          workspace_bytes: int, stream=None):
+    _check(load().tts_paged_decode_attn(
+        C.byref(desc), num_seqs, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_scale), _ptr(v_scale),
+        _ptr(block_tables), max_blocks_per_seq, _ptr(seq_lens), max_seq_len, num_blocks, _ptr(out), _ptr(workspace),
+        workspace_bytes, _stream(stream)))
+
+
+def tts_prefix_decode_attn(desc: tts_attn_desc, meta: PrefixMeta, q, k_cache, v_cache, k_scale, v_scale,
+                           block_tables, max_blocks_per_seq: int, seq_lens, num_blocks: int, out, workspace,
+                           workspace_bytes: int, stream=None):
+    _check(load().tts_prefix_decode_attn(
+        C.byref(desc), meta.handle, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_scale), _ptr(v_scale),
+        _ptr(block_tables), max_blocks_per_seq, _ptr(seq_lens), num_blocks, _ptr(out), _ptr(workspace),
+        workspace_bytes, _stream(stream)))
+

@@ -1,0 +1,244 @@
+"""GPU parity: libtts (through its C ABI) against the CPU oracle.
+
+Tolerances (max abs error of the fp32 outputs): 1e-4 for fp32 KV, 1e-2 for
+bf16 KV (bf16 operands, fp32 accumulation, probabilities rounded to bf16
+for the value product), 2e-2 for fp8 KV.
+"""
+
+import dataclasses
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.attention import oracle_attn_workload
+from oracle.prefix_meta import oracle_prefix_meta
+from paper_2509_00195_amd import TTSError
+from paper_2509_00195_amd.runner import PagedAttention, PrefixAttention
+from tts_synth import CONFIGS, AttnShape, BeamTree, make_workload, workload_from_tree
+from tts_synth.device import to_device
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 1e-2, "fp8": 2e-2}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a visible MI355X"
+    torch.cuda.set_device(0)
+
+
+def runners(wl, lens_for_meta=None):
+    x = to_device(wl)
+    paged = PagedAttention(x, wl.max_seq_len, wl.num_blocks)
+    pref = PrefixAttention(x, wl.req_seq_offsets, wl.block_tables,
+                           wl.seq_lens if lens_for_meta is None else lens_for_meta, wl.num_blocks)
+    return x, paged, pref
+
+
+def outputs(wl, lens_for_meta=None):
+    x, paged, pref = runners(wl, lens_for_meta)
+    op = paged().cpu().numpy()
+    ox = pref().cpu().numpy()
+    torch.cuda.synchronize()
+    return op, ox
+
+
+def err(a, b, rows=None):
+    if rows is not None:
+        a, b = a[rows], b[rows]
+    return float(np.max(np.abs(a.astype(np.float64) - b.astype(np.float64)))) if a.size else 0.0
+
+
+@pytest.mark.parametrize("name", ["tiny", "1p5b16", "7b64"])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_parity_configs(name, seed):
+    wl = make_workload(name, seed)
+    ref = oracle_attn_workload(wl)
+    op, ox = outputs(wl)
+    tol = TOL[wl.shape.kv_dtype]
+    print(f"{name} seed {seed}: paged {err(op, ref):.2e} prefix {err(ox, ref):.2e} (tol {tol})", flush=True)
+    assert np.isfinite(op).all() and np.isfinite(ox).all()
+    assert err(op, ref) <= tol
+    assert err(ox, ref) <= tol
+
+
+def test_parity_straggler():
+    wl = make_workload("7b_straggler", 0)
+    ref = oracle_attn_workload(wl)
+    op, ox = outputs(wl)
+    print(f"straggler: paged {err(op, ref):.2e} prefix {err(ox, ref):.2e}", flush=True)
+    assert err(op, ref) <= TOL["bf16"] and err(ox, ref) <= TOL["bf16"]
+
+
+def test_parity_longchain_fp8_sampled():
+    wl = make_workload("7b_longchain_fp8", 0)
+    s = wl.num_seqs
+    rng = np.random.default_rng(0)
+    rows = sorted(set(rng.choice(s, 20, replace=False).tolist()) | {int(np.argmax(wl.seq_lens)), 0, s - 1})
+    ref = oracle_attn_workload(wl, beams=rows)
+    op, ox = outputs(wl)
+    print(f"longchain fp8 ({len(rows)} beams): paged {err(op, ref, rows):.2e} prefix {err(ox, ref, rows):.2e}",
+          flush=True)
+    assert np.isfinite(op).all() and np.isfinite(ox).all()
+    assert err(op, ref, rows) <= TOL["fp8"] and err(ox, ref, rows) <= TOL["fp8"]
+    assert err(op, ox) <= TOL["fp8"]  # every beam: the two paths agree
+
+
+def test_run_to_run_deterministic():
+    wl = make_workload("7b64", 1)
+    x, paged, pref = runners(wl)
+    a1, b1 = paged().clone(), pref().clone()
+    a2, b2 = paged().clone(), pref().clone()
+    assert torch.equal(a1, a2) and torch.equal(b1, b2)
+
+
+def _duplicate_beams(wl, picks):
+    """Append exact copies (table, length, query) of the beams in `picks` to the last request."""
+    offs = wl.req_seq_offsets.copy()
+    offs[-1] += len(picks)
+    return dataclasses.replace(
+        wl, block_tables=np.vstack([wl.block_tables, wl.block_tables[picks]]),
+        seq_lens=np.concatenate([wl.seq_lens, wl.seq_lens[picks]]), q=np.concatenate([wl.q, wl.q[picks]]),
+        req_seq_offsets=offs)
+
+
+def test_identical_beams_bit_identical():
+    wl = make_workload("1p5b16", 0)
+    picks = [0, 5, 9]
+    wl2 = _duplicate_beams(wl, picks)
+    op, ox = outputs(wl2)
+    s = wl.num_seqs
+    for i, b in enumerate(picks):
+        assert np.array_equal(ox[b], ox[s + i])
+        assert np.array_equal(op[b], op[s + i])
+    ref = oracle_attn_workload(wl2)
+    assert err(ox, ref) <= TOL["bf16"]
+
+
+def test_physical_permutation_bit_exact():
+    wl = make_workload("1p5b16", 2)
+    op, ox = outputs(wl)
+    pi = np.random.default_rng(5).permutation(wl.num_blocks)
+    kc = np.empty_like(wl.k_cache)
+    vc = np.empty_like(wl.v_cache)
+    kc[pi] = wl.k_cache
+    vc[pi] = wl.v_cache
+    tables = np.where(wl.block_tables >= 0, pi[np.maximum(wl.block_tables, 0)], -1).astype(np.int32)
+    wl2 = dataclasses.replace(wl, k_cache=kc, v_cache=vc, block_tables=tables)
+    op2, ox2 = outputs(wl2)
+    assert np.array_equal(op, op2) and np.array_equal(ox, ox2)
+
+
+def _edge_tree():
+    """One request whose beams have lengths 0, 1, 15, 16, 17, 32, 33 and share prefixes,
+    a second request with a single beam, a third that is empty."""
+    t = BeamTree(block_size=16)
+    base = [t.new_alloc() for _ in range(3)]  # 48 tokens of shared prefix
+    specs = [(0, 0), (1, 1), (15, 1), (16, 1), (17, 2), (32, 2), (33, 3), (48, 3), (48, 3), (50, 4)]
+    for L, nshared in specs:
+        blocks = list(base[:min(nshared, L // 16)])
+        while len(blocks) * 16 < L:
+            blocks.append(t.new_alloc())
+        t.beam_allocs.append(blocks)
+        t.beam_lens.append(L)
+        t.beam_parent.append(-1)
+    t.req_offsets.append(len(t.beam_lens))
+    t.beam_allocs.append([t.new_alloc() for _ in range(7)])
+    t.beam_lens.append(100)
+    t.beam_parent.append(-1)
+    t.req_offsets.append(len(t.beam_lens))
+    t.req_offsets.append(len(t.beam_lens))  # empty request
+    return t
+
+
+@pytest.mark.parametrize("kv", ["bf16", "f32", "fp8"])
+def test_edge_lengths(kv):
+    shape = AttnShape(12, 2, 128, 16, "f32" if kv == "f32" else "bf16", kv)
+    wl = workload_from_tree(shape, _edge_tree(), 3, shuffle=False)
+    ref = oracle_attn_workload(wl)
+    op, ox = outputs(wl)
+    assert np.all(op[0] == 0) and np.all(ox[0] == 0)  # seq_len 0
+    assert err(op, ref) <= TOL[kv] and err(ox, ref) <= TOL[kv]
+    m = oracle_prefix_meta(wl.req_seq_offsets, wl.block_tables, wl.seq_lens, 16)
+    assert m["num_segs"] >= 2
+
+
+def test_head_dim_64_bf16():
+    cfg = CONFIGS["1p5b16"]
+    from tts_synth import build_tree
+    wl = workload_from_tree(AttnShape(16, 2, 64, 16, "bf16", "bf16"), build_tree(cfg, 4), 4)
+    ref = oracle_attn_workload(wl)
+    op, ox = outputs(wl)
+    assert err(op, ref) <= TOL["bf16"] and err(ox, ref) <= TOL["bf16"]
+
+
+def test_scale_override():
+    wl = make_workload("tiny", 1)
+    x = to_device(wl)
+    pref = PrefixAttention(x, wl.req_seq_offsets, wl.block_tables, wl.seq_lens, wl.num_blocks, scale=0.37)
+    paged = PagedAttention(x, wl.max_seq_len, wl.num_blocks, scale=0.37)
+    ref = oracle_attn_workload(wl, scale=0.37)
+    assert err(pref().cpu().numpy(), ref) <= 1e-4 and err(paged().cpu().numpy(), ref) <= 1e-4
+
+
+def test_private_appends_after_build():
+    """Metadata built at shorter lengths stays valid while beams only grow privately."""
+    wl = make_workload("7b64", 0)
+    m = oracle_prefix_meta(wl.req_seq_offsets, wl.block_tables, wl.seq_lens, 16)
+    short = np.maximum(m["tail_lblock"] * 16, wl.seq_lens - 37).astype(np.int32)
+    ref = oracle_attn_workload(wl)
+    _, ox = outputs(wl, lens_for_meta=short)
+    assert err(ox, ref) <= TOL["bf16"]
+
+
+def test_bad_block_id_gives_nan_row_only():
+    wl = make_workload("1p5b16", 0)
+    x, paged, pref = runners(wl)
+    good_p, good_x = paged().clone(), pref().clone()
+    m = oracle_prefix_meta(wl.req_seq_offsets, wl.block_tables, wl.seq_lens, 16)
+    b = 3
+    last = (int(wl.seq_lens[b]) + 15) // 16 - 1
+    assert last >= m["tail_lblock"][b]  # a tail block
+    x.block_tables[b, last] = wl.num_blocks + 1000
+    op, ox = paged(), pref()
+    torch.cuda.synchronize()
+    assert torch.isnan(op[b]).all() and torch.isnan(ox[b]).all()
+    others = [i for i in range(wl.num_seqs) if i != b]
+    assert torch.equal(op[others], good_p[others]) and torch.equal(ox[others], good_x[others])
+
+
+def test_stale_metadata_gives_nan_row():
+    wl = make_workload("1p5b16", 0)
+    x, paged, pref = runners(wl)
+    m = oracle_prefix_meta(wl.req_seq_offsets, wl.block_tables, wl.seq_lens, 16)
+    b = int(np.argmax(m["tail_lblock"]))
+    lens = x.seq_lens.clone()
+    lens[b] = int(m["tail_lblock"][b]) * 16 - 5
+    ox = pref(seq_lens=lens)
+    torch.cuda.synchronize()
+    assert torch.isnan(ox[b]).all()
+    assert torch.isfinite(ox[[i for i in range(wl.num_seqs) if i != b]]).all()
+
+
+def test_errors_from_device_calls():
+    wl = make_workload("tiny", 0)
+    x, paged, pref = runners(wl)
+    with pytest.raises(TTSError):  # workspace too small
+        from paper_2509_00195_amd import tts_prefix_decode_attn
+        tts_prefix_decode_attn(pref.desc, pref.meta, x.q, x.k_cache, x.v_cache, None, None, x.block_tables,
+                               x.block_tables.shape[1], x.seq_lens, wl.num_blocks, pref.out, pref.ws, 0)
+    with pytest.raises(TTSError):  # scales given for non-fp8 KV
+        from paper_2509_00195_amd import tts_paged_decode_attn
+        tts_paged_decode_attn(paged.desc, wl.num_seqs, x.q, x.k_cache, x.v_cache, x.seq_lens, x.seq_lens,
+                              x.block_tables, x.block_tables.shape[1], x.seq_lens, wl.max_seq_len, wl.num_blocks,
+                              paged.out, paged.ws, paged.ws_bytes)
+
+
+def test_work_plan_stats_and_workspace():
+    wl = make_workload("7b64", 0)
+    x, paged, pref = runners(wl)
+    units, slots = pref.meta.stats()
+    assert units > 0 and slots >= wl.num_seqs
+    assert pref.ws_bytes >= slots * wl.shape.num_q_heads * (wl.shape.head_dim + 2) * 4
