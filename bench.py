@@ -1,0 +1,260 @@
+"""Benchmark: prefix-shared beam decode attention on one MI355X.
+
+One step = one decode-attention call of one transformer layer for every beam
+of the batch (``tts_prefix_decode_attn``), i.e. one pass of the hot path
+over one batch. Steps rotate over ``--layers`` independent layer KV pools
+(same beam tree and block tables, different K/V values and queries), so the
+working set exceeds the 256 MB Infinity Cache and the timed KV reads come
+from HBM. The prefix metadata is built once per tree (once per reasoning
+step of the search); its host time is reported separately.
+
+Metric: beam-tokens/s = beams advanced by one token / time per layer call,
+plus the fraction of HBM peak achieved on the unique KV bytes of one call.
+
+Prints one JSON line. ``--gpus`` above 1 is refused: this build runs on one
+GPU.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "beam-tokens/s per decode step + % HBM peak (unique KV bytes), 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2509_00195_amd", "csrc", "tts_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def kernel_sha() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=560)
+    ap.add_argument("--warmup", type=int, default=56)
+    ap.add_argument("--config", default="7b64")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--layers", type=int, default=28)
+    ap.add_argument("--variant", choices=["prefix", "paged"], default="prefix")
+    ap.add_argument("--graph", action="store_true", help="replay the steps from a captured HIP graph")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--check", action="store_true", help="compare layer 0 against the oracle")
+    return ap.parse_args()
+
+
+def make_layers(wl, x, layers, seed):
+    """Per-layer K/V pools and queries: layer 0 is the generator's; others drawn on the GPU."""
+    import torch
+
+    sh = wl.shape
+    pools = [(x.q, x.k_cache, x.v_cache, x.k_scale, x.v_scale)]
+    g = torch.Generator(device=x.q.device)
+    g.manual_seed(1000 + seed)
+    for _ in range(1, layers):
+        def draw(shape, kind):
+            v = torch.randn(shape, generator=g, device=x.q.device, dtype=torch.float32)
+            if kind == "bf16":
+                return v.to(torch.bfloat16)
+            if kind == "fp8":
+                return v.clamp(-448, 448).to(torch.float8_e4m3fn).view(torch.uint8)
+            return v
+        q = draw(tuple(x.q.shape), sh.q_dtype)
+        k = draw(tuple(x.k_cache.shape), sh.kv_dtype)
+        v = draw(tuple(x.v_cache.shape), sh.kv_dtype)
+        ks = vs = None
+        if sh.kv_dtype == "fp8":
+            ks = torch.rand(wl.num_blocks, generator=g, device=x.q.device) * 0.01 + 0.001
+            vs = torch.rand(wl.num_blocks, generator=g, device=x.q.device) * 0.01 + 0.001
+        pools.append((q, k, v, ks, vs))
+    return pools
+
+
+def cpu_baseline(wl, budget_s):
+    """The oracle, as is, on the same batch: whole layer calls until the budget is used."""
+    from oracle.attention import oracle_attn_workload
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle_attn_workload(wl)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s or n >= 64:
+            break
+    per = el / n
+    return {"value": wl.num_seqs / per, "unit": "beam-tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} full layer calls of the {wl.name} batch ({wl.num_seqs} beams, all heads) "
+                      f"in {el:.1f} s on the host, numpy fp32 ({threads} BLAS threads)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2509_00195_amd import tts as T
+    from paper_2509_00195_amd.runner import PagedAttention, PrefixAttention
+    from tts_synth import CONFIGS, make_workload
+    from tts_synth.device import to_device
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = CONFIGS[args.config]
+    wl = make_workload(cfg, args.seed, poison=False)
+    sh = wl.shape
+    x = to_device(wl, dev)
+    # All work runs on one non-default stream (graph capture needs one);
+    # the timing events are recorded on it too.
+    stream = torch.cuda.Stream(device=dev)
+    torch.cuda.set_stream(stream)
+
+    t0 = time.perf_counter()
+    pref = PrefixAttention(x, wl.req_seq_offsets, wl.block_tables, wl.seq_lens, wl.num_blocks, stream=stream)
+    meta_ms = (time.perf_counter() - t0) * 1e3
+    view = pref.meta.export()
+    units, slots = pref.meta.stats()
+    eb = {"f32": 4, "bf16": 2, "fp8": 1}[sh.kv_dtype]
+    unique_kv = view["unique_tokens"] * sh.num_kv_heads * sh.head_dim * 2 * eb
+    if sh.kv_dtype == "fp8":
+        unique_kv += view["unique_blocks"] * 8
+    logical_tokens = int(wl.seq_lens.sum())
+    logical_kv = logical_tokens * sh.num_kv_heads * sh.head_dim * 2 * eb
+    paged = PagedAttention(x, wl.max_seq_len, wl.num_blocks)
+
+    pools = make_layers(wl, x, args.layers, args.seed)
+    out = pref.out
+    tabs, lens = x.block_tables, x.seq_lens
+    maxb = int(tabs.shape[1])
+
+    def step(i):
+        q, k, v, ks, vs = pools[i % len(pools)]
+        if args.variant == "prefix":
+            T.tts_prefix_decode_attn(pref.desc, pref.meta, q, k, v, ks, vs, tabs, maxb, lens, wl.num_blocks, out,
+                                     pref.ws, pref.ws_bytes, stream)
+        else:
+            T.tts_paged_decode_attn(paged.desc, wl.num_seqs, q, k, v, ks, vs, tabs, maxb, lens, wl.max_seq_len,
+                                    wl.num_blocks, out, paged.ws, paged.ws_bytes, stream)
+
+    check = None
+    if args.check:
+        from oracle.attention import oracle_attn_workload
+
+        step(0)
+        torch.cuda.synchronize()
+        ref = oracle_attn_workload(wl)
+        check = float(np.max(np.abs(out.cpu().numpy() - ref)))
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    graph = None
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=stream):
+            for i in range(len(pools)):
+                step(i)
+        graph.replay()
+        torch.cuda.synchronize()
+
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    if graph is not None:
+        reps = max(1, args.steps // len(pools))
+        for _ in range(reps):
+            graph.replay()
+        steps = reps * len(pools)
+    else:
+        for i in range(args.steps):
+            step(i)
+        steps = args.steps
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end)
+    ms_per_step = ms / steps
+    value = wl.num_seqs / (ms_per_step * 1e-3)
+
+    kv_bytes = unique_kv if args.variant == "prefix" else logical_kv
+    achieved = kv_bytes / (ms_per_step * 1e-3) / 1e9
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        key = f"{args.config}:{args.variant}"
+        if tr.get("kernel_sha") == kernel_sha() and key in tr.get("entries", {}):
+            traffic = tr["entries"][key]["bytes_per_launch"]
+
+    rec = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "beam-tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": sh.kv_dtype,
+        "data": "synthetic (seeded beam-search tree; random K/V/Q)",
+        "config": {
+            "workload": f"{args.config}: {cfg.description}",
+            "seed": args.seed,
+            "variant": args.variant,
+            "beams": wl.num_seqs,
+            "layers_rotated": len(pools),
+            "graph_replay": bool(args.graph),
+            "unique_kv_bytes": int(unique_kv),
+            "logical_kv_bytes": int(logical_kv),
+            "sharing": logical_kv / max(unique_kv, 1),
+            "unique_kv_hbm_frac": unique_kv / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
+            "per_28_layer_step_beam_tokens_per_s": value / 28.0,
+            "work_units": units,
+            "partial_slots": slots,
+            "meta_build_ms": meta_ms,
+            "max_abs_err_vs_oracle": check,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+        },
+    }
+    if not args.no_cpu_baseline:
+        wl_cpu = make_workload(cfg, args.seed, poison=False)
+        rec["cpu_baseline"] = cpu_baseline(wl_cpu, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

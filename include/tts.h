@@ -171,7 +171,8 @@ size_t tts_paged_decode_workspace_size(const tts_attn_desc* d, int32_t num_seqs,
  * sequences); beams longer than it get NaN rows.
  * num_blocks: size of the block pool (ids outside it give NaN rows).
  * workspace: device buffer of at least tts_paged_decode_workspace_size
- * bytes (TTS_ERR_WORKSPACE otherwise); NULL allowed when that size is 0. */
+ * bytes (TTS_ERR_WORKSPACE otherwise); NULL allowed when that size is 0.
+ * Calls that overlap in time must not share a workspace. */
 tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const void* q, const void* k_cache,
                                  const void* v_cache, const float* k_scale, const float* v_scale,
                                  const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
@@ -191,7 +192,8 @@ size_t tts_prefix_decode_workspace_size(const tts_attn_desc* d, const tts_prefix
  * still valid: every table entry a segment covers is unchanged and every
  * seq_len is >= its value at build time (beams only appended privately).
  * block_tables/seq_lens: device copies of the current tables and lengths.
- * workspace: at least tts_prefix_decode_workspace_size bytes. */
+ * workspace: at least tts_prefix_decode_workspace_size bytes (partial
+ * softmax states; calls that overlap in time must not share one). */
 tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
                                   const void* k_cache, const void* v_cache, const float* k_scale,
                                   const float* v_scale, const int32_t* block_tables, int32_t max_blocks_per_seq,

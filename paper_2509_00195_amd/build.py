@@ -22,6 +22,7 @@ LIB = os.path.join(PKG, "libtts.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
+
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 SOURCES_HIP = ["tts_kernels.hip"]
@@ -36,25 +37,27 @@ def _run(cmd):
     return r
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link libtts.so; returns its path."""
+def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+    """Compile every source and link libtts.so (or ``out``); returns its path.
+
+    ``defines`` adds preprocessor definitions (tuning builds only)."""
     with tempfile.TemporaryDirectory(prefix="tts_build_") as tmp:
         objs = []
         for src in SOURCES_HIP:
             obj = os.path.join(tmp, src + ".o")
-            _run([HIPCC, *COMMON, *DEVICE, "-c", os.path.join(CSRC, src), "-o", obj])
+            _run([HIPCC, *COMMON, *[f"-D{d}" for d in defines], *DEVICE, "-c", os.path.join(CSRC, src), "-o", obj])
             objs.append(obj)
         for src in SOURCES_HOST:
             obj = os.path.join(tmp, src + ".o")
-            _run([HIPCC, *COMMON, "-c", os.path.join(CSRC, src), "-o", obj])
+            _run([HIPCC, *COMMON, *[f"-D{d}" for d in defines], "-c", os.path.join(CSRC, src), "-o", obj])
             objs.append(obj)
         out_tmp = os.path.join(tmp, "libtts.so")
         _run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", out_tmp])
-        shutil.copyfile(out_tmp, LIB + ".tmp")
-        os.replace(LIB + ".tmp", LIB)
+        shutil.copyfile(out_tmp, out + ".tmp")
+        os.replace(out + ".tmp", out)
     if verbose:
-        print(f"built {LIB}")
-    return LIB
+        print(f"built {out}")
+    return out
 
 
 if __name__ == "__main__":

@@ -2,6 +2,7 @@
 // and kernel launches.
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -9,7 +10,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/tts.h"
+#include "tts.h"
 #include "tts_meta.h"
 #include "tts_work.h"
 
@@ -260,6 +261,7 @@ tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const
   p.part_o = ns > 1 ? static_cast<float*>(workspace) : nullptr;
   p.part_ml = ns > 1 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * d->head_dim * 4))
                      : nullptr;
+
   p.max_blocks = max_blocks_per_seq;
   p.num_blocks = num_blocks;
   p.num_seqs = num_seqs;
@@ -277,14 +279,11 @@ tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const
     tts::MergeParams mp{};
     mp.part_o = p.part_o;
     mp.part_ml = p.part_ml;
-    mp.slot_base = nullptr;
     mp.seq_lens = seq_lens;
-    mp.tail_lblock = nullptr;
     mp.out = p.out;
     mp.num_seqs = num_seqs;
     mp.hq = d->num_q_heads;
     mp.paged_nsplit = ns;
-    mp.block_size = 16;
     e = tts::launch_merge(mp, d->head_dim, stream);
     if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
   }
@@ -333,6 +332,7 @@ tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta*
   p.out = static_cast<float*>(out);
   p.part_o = static_cast<float*>(workspace);
   p.part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * d->head_dim * 4));
+
   p.perm = reinterpret_cast<const int32_t*>(dev + m->off_perm);
   p.tail_lblock = reinterpret_cast<const int32_t*>(dev + m->off_tail);
   p.slot_base = reinterpret_cast<const int32_t*>(dev + m->off_slot);
@@ -359,11 +359,18 @@ tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta*
   mp.out = p.out;
   mp.num_seqs = S;
   mp.hq = d->num_q_heads;
-  mp.paged_nsplit = 0;
-  mp.block_size = 16;
   e = tts::launch_merge(mp, d->head_dim, stream);
   if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
   return ok();
 }
+
+#ifdef TTS_PROFILE_UNITS
+// Tuning builds only: copy the work list of a handle (12 int32 per unit).
+int64_t tts_prof_units(const tts_prefix_meta* m, int32_t* out, int64_t cap) {
+  const int64_t n = static_cast<int64_t>(m->plan.units.size());
+  if (out) std::memcpy(out, m->plan.units.data(), sizeof(tts::Unit) * static_cast<size_t>(std::min(n, cap)));
+  return n;
+}
+#endif
 
 }  // extern "C"

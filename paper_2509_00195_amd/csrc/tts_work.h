@@ -7,7 +7,8 @@
 
 namespace tts {
 
-// Rows of one KV head handled by one workgroup: 4 waves x 16 rows.
+// Rows of one KV head handled by one workgroup: 4 waves x 16 rows, cut at
+// whole beams (a unit covers floor(64 / g) beams).
 constexpr int kRowsPerUnit = 64;
 constexpr int kUnitInts = 12;
 
@@ -24,7 +25,7 @@ enum UnitKind : int32_t { kSegmentPiece = 0, kTailSplit = 1 };
 // private blocks [tail_lblock, ceil(seq_len / block_size)), from the live
 // block table (last block possibly partial).
 // Output: a partial softmax state written to slot `slot` of every covered
-// beam (slot order = merge order).
+// beam (slot order = merge order). A unit with nrows == 0 is padding.
 struct Unit {
   int32_t kvh;
   int32_t kind;
@@ -68,17 +69,18 @@ struct AttnParams {
   int32_t pad;
 };
 
+
 struct MergeParams {
   const float* part_o;
   const float* part_ml;
-  const int32_t* slot_base;  // [S + 1]; null for the paged path
+  const int32_t* slot_base;    // [S + 1]; null for the paged path
   const int32_t* seq_lens;
-  const int32_t* tail_lblock; // prefix path: stale-metadata check
+  const int32_t* tail_lblock;  // prefix path: stale-metadata check (else null)
   float* out;
   int32_t num_seqs;
   int32_t hq;
   int32_t paged_nsplit;
-  int32_t block_size;
+  int32_t pad;
 };
 
 }  // namespace tts

@@ -69,6 +69,12 @@ def load() -> C.CDLL:
         return _lib
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} not built: run __graft_entry__.build() or python -m paper_2509_00195_amd.build")
+    # Bind to the HIP runtime PyTorch already uses (same soname): the caller's
+    # device memory and streams come from it.
+    try:
+        import torch  # noqa: F401
+    except ImportError:  # pragma: no cover - C callers without torch
+        pass
     lib = C.CDLL(LIB_PATH)
     P, I32, I64, VP = C.POINTER, C.c_int32, C.c_int64, C.c_void_p
     pi32 = P(C.c_int32)
@@ -156,8 +162,8 @@ class PrefixMeta:
         self.destroy()
 
     def destroy(self):
-        if getattr(self, "handle", None):
-            tts_prefix_meta_destroy(self)
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.tts_prefix_meta_destroy(self.handle)
             self.handle = None
 
     def export(self) -> dict:
