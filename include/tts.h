@@ -200,6 +200,23 @@ tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta*
                                   const int32_t* seq_lens, int32_t num_blocks, void* out, void* workspace,
                                   size_t workspace_bytes, hipStream_t stream);
 
+/* The two launches of tts_prefix_decode_attn, for callers that schedule
+ * them separately (to overlap the merge with other work, or to time the
+ * attention kernel alone). tts_prefix_decode_partials runs the work units
+ * and leaves one partial softmax state (running max, sum, unnormalised
+ * output row) per (beam, query head, slot) in the workspace;
+ * tts_prefix_decode_merge combines each beam's states, in slot order, into
+ * out. Arguments and rules are those of tts_prefix_decode_attn; the merge
+ * must follow the partials call on the same workspace in stream order, with
+ * the same metadata and seq_lens. */
+tts_status tts_prefix_decode_partials(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
+                                      const void* k_cache, const void* v_cache, const float* k_scale,
+                                      const float* v_scale, const int32_t* block_tables,
+                                      int32_t max_blocks_per_seq, const int32_t* seq_lens, int32_t num_blocks,
+                                      void* out, void* workspace, size_t workspace_bytes, hipStream_t stream);
+tts_status tts_prefix_decode_merge(const tts_attn_desc* d, const tts_prefix_meta* m, const int32_t* seq_lens,
+                                   void* out, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Thread-local text of the last error ("" if none). */
 const char* tts_last_error(void);
 

@@ -296,71 +296,122 @@ size_t tts_prefix_decode_workspace_size(const tts_attn_desc* d, const tts_prefix
   return align256(rows * d->head_dim * 4) + align256(rows * 2 * 4);
 }
 
-tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
-                                  const void* k_cache, const void* v_cache, const float* k_scale,
-                                  const float* v_scale, const int32_t* block_tables, int32_t max_blocks_per_seq,
-                                  const int32_t* seq_lens, int32_t num_blocks, void* out, void* workspace,
-                                  size_t workspace_bytes, hipStream_t stream) {
+namespace {
+
+// Validation shared by the prefix-path entry points; fills the kernel
+// parameters on success.
+tts_status prefix_params(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q, const void* k_cache,
+                         const void* v_cache, const float* k_scale, const float* v_scale,
+                         const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                         int32_t num_blocks, void* out, void* workspace, size_t workspace_bytes, bool need_kv,
+                         tts::AttnParams* p) {
   tts_status s = check_desc(d);
   if (s != TTS_OK) return s;
-  if ((s = check_scales(d, k_scale, v_scale)) != TTS_OK) return s;
+  if (need_kv && (s = check_scales(d, k_scale, v_scale)) != TTS_OK) return s;
   if (!m) return fail(TTS_ERR_INVALID_ARG, "metadata is NULL");
   if (!m->has_plan || !m->dev) return fail(TTS_ERR_INVALID_ARG, "metadata was built without a desc");
   if (m->desc.num_q_heads != d->num_q_heads || m->desc.num_kv_heads != d->num_kv_heads ||
       m->desc.head_dim != d->head_dim)
     return fail(TTS_ERR_INVALID_ARG, "desc shape differs from the one the metadata was built for");
-  if (max_blocks_per_seq != m->host.max_blocks)
-    return fail(TTS_ERR_INVALID_ARG, "max_blocks_per_seq differs from the metadata's");
-  if (num_blocks < m->num_blocks) return fail(TTS_ERR_INVALID_ARG, "num_blocks smaller than at build time");
+  if (need_kv) {
+    if (max_blocks_per_seq != m->host.max_blocks)
+      return fail(TTS_ERR_INVALID_ARG, "max_blocks_per_seq differs from the metadata's");
+    if (num_blocks < m->num_blocks) return fail(TTS_ERR_INVALID_ARG, "num_blocks smaller than at build time");
+  }
   const int32_t S = m->host.num_seqs;
-  if (S == 0) return ok();
-  if (!q || !k_cache || !v_cache || !block_tables || !seq_lens || !out)
+  if (S == 0) return TTS_OK;
+  if (!seq_lens || !out || (need_kv && (!q || !k_cache || !v_cache || !block_tables)))
     return fail(TTS_ERR_INVALID_ARG, "NULL device pointer");
   const size_t need = tts_prefix_decode_workspace_size(d, m);
   if (!workspace || workspace_bytes < need)
     return fail(TTS_ERR_WORKSPACE, "workspace smaller than tts_prefix_decode_workspace_size");
   const size_t rows = static_cast<size_t>(m->plan.num_slots) * d->num_q_heads;
   const char* dev = static_cast<const char*>(m->dev);
-  tts::AttnParams p{};
-  p.q = q;
-  p.k_cache = k_cache;
-  p.v_cache = v_cache;
-  p.k_scale = k_scale;
-  p.v_scale = v_scale;
-  p.block_tables = block_tables;
-  p.seq_lens = seq_lens;
-  p.out = static_cast<float*>(out);
-  p.part_o = static_cast<float*>(workspace);
-  p.part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * d->head_dim * 4));
+  *p = tts::AttnParams{};
+  p->q = q;
+  p->k_cache = k_cache;
+  p->v_cache = v_cache;
+  p->k_scale = k_scale;
+  p->v_scale = v_scale;
+  p->block_tables = block_tables;
+  p->seq_lens = seq_lens;
+  p->out = static_cast<float*>(out);
+  p->part_o = static_cast<float*>(workspace);
+  p->part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * d->head_dim * 4));
+  p->perm = reinterpret_cast<const int32_t*>(dev + m->off_perm);
+  p->tail_lblock = reinterpret_cast<const int32_t*>(dev + m->off_tail);
+  p->slot_base = reinterpret_cast<const int32_t*>(dev + m->off_slot);
+  p->seg_blocks = reinterpret_cast<const int32_t*>(dev + m->off_seg);
+  p->units = reinterpret_cast<const tts::Unit*>(dev + m->off_units);
+  p->max_blocks = max_blocks_per_seq;
+  p->num_blocks = num_blocks;
+  p->num_seqs = S;
+  p->hq = d->num_q_heads;
+  p->hkv = d->num_kv_heads;
+  p->g = d->num_q_heads / d->num_kv_heads;
+  p->scale_log2 = scale_log2(d);
+  return TTS_OK;
+}
 
-  p.perm = reinterpret_cast<const int32_t*>(dev + m->off_perm);
-  p.tail_lblock = reinterpret_cast<const int32_t*>(dev + m->off_tail);
-  p.slot_base = reinterpret_cast<const int32_t*>(dev + m->off_slot);
-  p.seg_blocks = reinterpret_cast<const int32_t*>(dev + m->off_seg);
-  p.units = reinterpret_cast<const tts::Unit*>(dev + m->off_units);
-  p.max_blocks = max_blocks_per_seq;
-  p.num_blocks = num_blocks;
-  p.num_seqs = S;
-  p.hq = d->num_q_heads;
-  p.hkv = d->num_kv_heads;
-  p.g = d->num_q_heads / d->num_kv_heads;
-  p.scale_log2 = scale_log2(d);
-  p.paged_nsplit = 0;
-  p.paged_max_len = 0;
+tts_status launch_partials(const tts_attn_desc* d, const tts_prefix_meta* m, const tts::AttnParams& p,
+                           hipStream_t stream) {
   hipError_t e =
       tts::launch_attn_units(p, static_cast<int>(m->plan.units.size()), d->head_dim, kv_kind(d), stream);
   if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("attention launch: ") + hipGetErrorString(e));
+  return TTS_OK;
+}
+
+tts_status launch_prefix_merge(const tts_attn_desc* d, const tts::AttnParams& p, hipStream_t stream) {
   tts::MergeParams mp{};
   mp.part_o = p.part_o;
   mp.part_ml = p.part_ml;
   mp.slot_base = p.slot_base;
-  mp.seq_lens = seq_lens;
+  mp.seq_lens = p.seq_lens;
   mp.tail_lblock = p.tail_lblock;
   mp.out = p.out;
-  mp.num_seqs = S;
+  mp.num_seqs = p.num_seqs;
   mp.hq = d->num_q_heads;
-  e = tts::launch_merge(mp, d->head_dim, stream);
+  hipError_t e = tts::launch_merge(mp, d->head_dim, stream);
   if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
+  return TTS_OK;
+}
+
+}  // namespace
+
+tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
+                                  const void* k_cache, const void* v_cache, const float* k_scale,
+                                  const float* v_scale, const int32_t* block_tables, int32_t max_blocks_per_seq,
+                                  const int32_t* seq_lens, int32_t num_blocks, void* out, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  tts::AttnParams p;
+  tts_status s = prefix_params(d, m, q, k_cache, v_cache, k_scale, v_scale, block_tables, max_blocks_per_seq,
+                               seq_lens, num_blocks, out, workspace, workspace_bytes, true, &p);
+  if (s != TTS_OK || m->host.num_seqs == 0) return s == TTS_OK ? ok() : s;
+  if ((s = launch_partials(d, m, p, stream)) != TTS_OK) return s;
+  if ((s = launch_prefix_merge(d, p, stream)) != TTS_OK) return s;
+  return ok();
+}
+
+tts_status tts_prefix_decode_partials(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
+                                      const void* k_cache, const void* v_cache, const float* k_scale,
+                                      const float* v_scale, const int32_t* block_tables,
+                                      int32_t max_blocks_per_seq, const int32_t* seq_lens, int32_t num_blocks,
+                                      void* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  tts::AttnParams p;
+  tts_status s = prefix_params(d, m, q, k_cache, v_cache, k_scale, v_scale, block_tables, max_blocks_per_seq,
+                               seq_lens, num_blocks, out, workspace, workspace_bytes, true, &p);
+  if (s != TTS_OK || m->host.num_seqs == 0) return s == TTS_OK ? ok() : s;
+  if ((s = launch_partials(d, m, p, stream)) != TTS_OK) return s;
+  return ok();
+}
+
+tts_status tts_prefix_decode_merge(const tts_attn_desc* d, const tts_prefix_meta* m, const int32_t* seq_lens,
+                                   void* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  tts::AttnParams p;
+  tts_status s = prefix_params(d, m, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, seq_lens, 0, out,
+                               workspace, workspace_bytes, false, &p);
+  if (s != TTS_OK || m->host.num_seqs == 0) return s == TTS_OK ? ok() : s;
+  if ((s = launch_prefix_merge(d, p, stream)) != TTS_OK) return s;
   return ok();
 }
 

@@ -164,14 +164,18 @@ __device__ __forceinline__ void pair_step(const PairFrags<D, KV>& f, const void*
   }
   // Lane (ln, lq) holds row ln, tokens 8*lq + 4*t + i of the pair; they all
   // lie in block lq >> 1 of the pair, at slots 8*(lq & 1) + 4*t + i.
+  // bf16/fp32 scores stay unscaled (their scale is positive, so it
+  // preserves the maximum) and the scale is applied inside the exponent:
+  // p = 2^(acc * sc - m).
   const bool hi = lq >= 2;
   const float sc = hi ? sc1 : sc0;
-  const float vs = hi ? vs1 : vs0;
+  // fp8 block scales are caller data (any sign): scale first there.
+  constexpr bool kPreScale = KV == kKvFp8;
   float s[8];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) s[4 * t + i] = acc[t][i] * sc;
+    for (int i = 0; i < 4; ++i) s[4 * t + i] = kPreScale ? acc[t][i] * sc : acc[t][i];
   if (masked) {
     const int valid = hi ? valid1 : valid0;
     const int slot0 = 8 * (lq & 1);
@@ -181,10 +185,11 @@ __device__ __forceinline__ void pair_step(const PairFrags<D, KV>& f, const void*
       for (int i = 0; i < 4; ++i)
         if (slot0 + 4 * t + i >= valid) s[4 * t + i] = kNegInf;
   }
-  float lmax = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
-  if (__builtin_amdgcn_ballot_w64(lmax > st.m + kRescale) != 0) {
+  float smax = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
+  const float lm = kPreScale ? smax : smax * sc;  // largest scaled score of this lane (-inf if all masked)
+  if (__builtin_amdgcn_ballot_w64(lm > st.m + kRescale) != 0) {
     // Rare: move the reference maximum up for every row of the wave.
-    const float rmax = xlane_max16(lmax);
+    const float rmax = xlane_max16(lm);
     const float m_new = fmaxf(st.m, rmax);
     const float alpha = (st.m == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(st.m - m_new);
     st.l *= alpha;
@@ -195,7 +200,7 @@ __device__ __forceinline__ void pair_step(const PairFrags<D, KV>& f, const void*
   const float mu = (st.m == kNegInf) ? 0.f : st.m;
   float p[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) p[i] = __builtin_amdgcn_exp2f(s[i] - mu);
+  for (int i = 0; i < 8; ++i) p[i] = __builtin_amdgcn_exp2f(kPreScale ? s[i] - mu : __builtin_fmaf(s[i], sc, -mu));
   st.l += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
   if constexpr (F::f32) {
 #pragma unroll
@@ -213,8 +218,11 @@ __device__ __forceinline__ void pair_step(const PairFrags<D, KV>& f, const void*
       st.o[dt] = o;
     }
   } else {
-    const uint4 pb = {pack_bf16x2(p[0] * vs, p[1] * vs), pack_bf16x2(p[2] * vs, p[3] * vs),
-                      pack_bf16x2(p[4] * vs, p[5] * vs), pack_bf16x2(p[6] * vs, p[7] * vs)};
+    float pv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) pv[i] = (KV == kKvFp8) ? p[i] * (hi ? vs1 : vs0) : p[i];
+    const uint4 pb = {pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]), pack_bf16x2(pv[4], pv[5]),
+                      pack_bf16x2(pv[6], pv[7])};
     const bf16x8 pbf = __builtin_bit_cast(bf16x8, pb);
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt)
@@ -797,15 +805,15 @@ __global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(AttnParams p) {
 // Exact merge of the partial softmax states of each (beam, query head), in
 // slot order (segments root to leaf, then tail splits):
 //   m = max_k m_k,  l = sum_k l_k 2^(m_k - m),  out = sum_k o_k 2^(m_k - m) / l.
-// kTpr threads share a row (8 output dims each); every thread issues the
-// loads of up to kBatch slots before combining them.
+// D/4 threads share a row (4 output dims each) and issue the loads of up to
+// kBatch slots at once, so a row costs one round trip to memory per batch.
 template <int D>
 __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
-  constexpr int kTpr = D / 8;
+  constexpr int kTpr = D / 4;
   constexpr int kRows = kThreads / kTpr;
-  constexpr int kBatch = 8;
+  constexpr int kBatch = 16;
   const int r = blockIdx.x * kRows + threadIdx.x / kTpr;
-  const int d0 = (threadIdx.x % kTpr) * 8;
+  const int d0 = (threadIdx.x % kTpr) * 4;
   if (r >= p.num_seqs * p.hq) return;
   const int b = r / p.hq;
   const int h = r % p.hq;
@@ -821,19 +829,20 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
   const int L = p.seq_lens[b];
   bool nan = p.tail_lblock && L < p.tail_lblock[b] * kTok;
   float mx = kNegInf, l = 0.f;
-  f32x4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int k0 = 0; k0 < n; k0 += kBatch) {
     f32x2 ml[kBatch];
-    f32x4 o0[kBatch], o1[kBatch];
+    f32x4 o[kBatch];
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
       const int kk = k0 + k < n ? k0 + k : n - 1;
       const int64_t row = (base + kk) * p.hq + h;
       ml[k] = *reinterpret_cast<const f32x2*>(p.part_ml + row * 2);
-      o0[k] = *reinterpret_cast<const f32x4*>(p.part_o + row * D + d0);
-      o1[k] = *reinterpret_cast<const f32x4*>(p.part_o + row * D + d0 + 4);
-      if (k0 + k >= n) ml[k] = f32x2{kNegInf, 0.f};
+      o[k] = *reinterpret_cast<const f32x4*>(p.part_o + row * D + d0);
     }
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k)
+      if (k0 + k >= n) ml[k] = f32x2{kNegInf, 0.f};
     float bm = kNegInf;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
@@ -844,27 +853,22 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
     if (mn == kNegInf) continue;
     const float a = (mx == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(mx - mn);
     l *= a;
-    acc0 *= a;
-    acc1 *= a;
+    acc *= a;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
       const float fct = (ml[k].x == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(ml[k].x - mn);
       l += ml[k].y * fct;
-      acc0 += o0[k] * fct;
-      acc1 += o1[k] * fct;
+      acc += o[k] * fct;
     }
     mx = mn;
   }
   const float inv = (l > 0.f && L > 0) ? 1.f / l : 0.f;
-  f32x4 w0 = acc0 * inv, w1 = acc1 * inv;
+  f32x4 w = acc * inv;
   if (nan) {
     const float q = __builtin_nanf("");
-    w0 = f32x4{q, q, q, q};
-    w1 = w0;
+    w = f32x4{q, q, q, q};
   }
-  float* orow = p.out + static_cast<int64_t>(r) * D + d0;
-  *reinterpret_cast<f32x4*>(orow) = w0;
-  *reinterpret_cast<f32x4*>(orow + 4) = w1;
+  *reinterpret_cast<f32x4*>(p.out + static_cast<int64_t>(r) * D + d0) = w;
 }
 
 template <int D, int KV>
@@ -876,7 +880,7 @@ static hipError_t launch_attn_t(const AttnParams& p, int num_units, hipStream_t 
 hipError_t launch_merge(const MergeParams& p, int head_dim, hipStream_t stream) {
   const int rows = p.num_seqs * p.hq;
   if (rows <= 0) return hipSuccess;
-  const int per = kThreads / (head_dim / 8);
+  const int per = kThreads / (head_dim / 4);
   const int blocks = (rows + per - 1) / per;
   if (head_dim == 128)
     hipLaunchKernelGGL((merge_kernel<128>), dim3(blocks), dim3(kThreads), 0, stream, p);

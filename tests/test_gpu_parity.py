@@ -242,3 +242,17 @@ def test_work_plan_stats_and_workspace():
     units, slots = pref.meta.stats()
     assert units > 0 and slots >= wl.num_seqs
     assert pref.ws_bytes >= slots * wl.shape.num_q_heads * (wl.shape.head_dim + 2) * 4
+
+
+def test_partials_then_merge_equals_single_call():
+    from paper_2509_00195_amd import tts_prefix_decode_merge, tts_prefix_decode_partials
+
+    wl = make_workload("7b64", 2)
+    x, paged, pref = runners(wl)
+    ref = pref().clone()
+    out = torch.full_like(ref, float("nan"))
+    tts_prefix_decode_partials(pref.desc, pref.meta, x.q, x.k_cache, x.v_cache, None, None, x.block_tables,
+                               x.block_tables.shape[1], x.seq_lens, wl.num_blocks, out, pref.ws, pref.ws_bytes)
+    tts_prefix_decode_merge(pref.desc, pref.meta, x.seq_lens, out, pref.ws, pref.ws_bytes)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
