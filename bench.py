@@ -54,6 +54,13 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--check", action="store_true", help="compare layer 0 against the oracle")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after the timed region, stream this many MiB device-to-device three times with a plain "
+                         "elementwise copy (dst = ~src; counter calibration runs)")
+    ap.add_argument("--ingest-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="read two rocprofv3 counter_collection.csv files (FETCH_SIZE run, WRITE_SIZE run, both "
+                         "made with --copy-mib) and record the attention kernel's HBM bytes per launch in "
+                         "profiles/traffic.json; runs no GPU work")
     return ap.parse_args()
 
 
@@ -108,8 +115,59 @@ def cpu_baseline(wl, budget_s):
                       f"in {el:.1f} s on the host, numpy fp32 ({threads} BLAS threads)"}
 
 
+COPY_KERNEL = "bitwise_not"  # the calibration copy: dst = ~src, one read and one write per byte
+ATTN_KERNEL = "attn_units_kernel"
+
+
+def _counter_rows(path, counter):
+    import csv
+
+    with open(path, newline="") as f:
+        return [r for r in csv.DictReader(f) if r["Counter_Name"] == counter]
+
+
+def ingest_traffic(args):
+    """HBM bytes per attention launch from FETCH_SIZE / WRITE_SIZE counter runs.
+
+    Each counter (KiB per dispatch) is scaled by bytes / counter of the plain
+    copy kernel of ``--copy-mib`` MiB (read once, written once) recorded in
+    the same run, then averaged over every attention dispatch."""
+    if args.copy_mib <= 0:
+        raise SystemExit("--ingest-traffic needs the --copy-mib the counter runs used")
+    copy_kib = args.copy_mib * 1024.0
+    rec = {"kernel_sha": kernel_sha(), "entries": {}}
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            old = json.load(f)
+        if old.get("kernel_sha") == rec["kernel_sha"]:
+            rec = old
+    ent = {"copy_mib": args.copy_mib}
+    total = 0.0
+    for path, counter in zip(args.ingest_traffic, ("FETCH_SIZE", "WRITE_SIZE")):
+        rows = _counter_rows(path, counter)
+        attn = [float(r["Counter_Value"]) for r in rows if ATTN_KERNEL in r["Kernel_Name"]]
+        copy = [float(r["Counter_Value"]) for r in rows if COPY_KERNEL in r["Kernel_Name"]
+                and int(r["Grid_Size"]) > 0]
+        if not attn or not copy:
+            raise SystemExit(f"{path}: no {ATTN_KERNEL} or {COPY_KERNEL} dispatches with {counter}")
+        copy_kib_meas = copy[-1]  # the last copy dispatches are the calibration copies
+        factor = copy_kib / copy_kib_meas
+        kib = float(np.mean(attn))
+        ent[counter.lower()] = {"attn_kib_mean": kib, "attn_dispatches": len(attn), "copy_kib": copy_kib_meas,
+                                "factor": factor}
+        total += kib * factor * 1024.0
+    ent["bytes_per_launch"] = total
+    rec["entries"][f"{args.config}:{args.variant}"] = ent
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(ent))
+
+
 def main():
     args = parse()
+    if args.ingest_traffic:
+        ingest_traffic(args)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path",
               file=sys.stderr)
@@ -264,6 +322,12 @@ def main():
             "traffic": traffic,
         },
     }
+    if args.copy_mib > 0:
+        src = torch.ones(args.copy_mib << 20, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.bitwise_not(src, out=dst)
+        torch.cuda.synchronize()
     if not args.no_cpu_baseline:
         wl_cpu = make_workload(cfg, args.seed, poison=False)
         rec["cpu_baseline"] = cpu_baseline(wl_cpu, args.cpu_seconds)
