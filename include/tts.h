@@ -42,10 +42,13 @@
  *   slots of a partially filled last block.
  * - FP8 KV: OCP E4M3FN codes; the value of a code in block p is
  *   decode(code) * k_scale[p] (keys) or * v_scale[p] (values).
- * - Device-side errors: a block id outside [0, num_blocks), a sequence
- *   longer than its table row, or (prefix call) a beam shorter than the
- *   metadata was built for makes that beam's output row NaN; no memory
- *   outside the given buffers is touched.
+ * - Device-side errors: a block id outside [0, num_blocks) read from a
+ *   device table (any entry in the paged call; an entry appended after the
+ *   metadata was built in the prefix call -- entries in use at build time
+ *   are validated by tts_build_prefix_meta), a sequence longer than its
+ *   table row, or (prefix call) a beam shorter than the metadata was built
+ *   for makes that beam's output row NaN; no memory outside the given
+ *   buffers is touched.
  */
 #ifndef TTS_H_
 #define TTS_H_
@@ -189,8 +192,10 @@ size_t tts_prefix_decode_workspace_size(const tts_attn_desc* d, const tts_prefix
  * combined by an exact log-sum-exp merge in a fixed order. Same result as
  * tts_paged_decode_attn up to rounding.
  * m: built with the same desc shape and with the same block tables, and
- * still valid: every table entry a segment covers is unchanged and every
- * seq_len is >= its value at build time (beams only appended privately).
+ * still valid: every table entry in use at build time is unchanged and
+ * every seq_len is >= its value at build time (beams only appended
+ * privately). The ids of the blocks in use at build time are taken from
+ * the metadata; blocks appended since are read from block_tables.
  * block_tables/seq_lens: device copies of the current tables and lengths.
  * workspace: at least tts_prefix_decode_workspace_size bytes (partial
  * softmax states; calls that overlap in time must not share one). */

@@ -15,7 +15,7 @@
 #include "tts_work.h"
 
 namespace tts {
-hipError_t launch_attn_units(const AttnParams& p, int num_units, int head_dim, int kv_kind, hipStream_t stream);
+hipError_t launch_attn(const AttnParams& p, int grid, int head_dim, int kv_kind, hipStream_t stream);
 hipError_t launch_merge(const MergeParams& p, int head_dim, hipStream_t stream);
 }  // namespace tts
 
@@ -40,7 +40,7 @@ tts_status check_desc(const tts_attn_desc* d) {
   if (!d) return fail(TTS_ERR_INVALID_ARG, "desc is NULL");
   if (d->num_q_heads <= 0 || d->num_kv_heads <= 0 || d->num_q_heads % d->num_kv_heads != 0)
     return fail(TTS_ERR_INVALID_ARG, "num_q_heads must be a positive multiple of num_kv_heads");
-  if (d->num_q_heads / d->num_kv_heads > tts::kRowsPerUnit)
+  if (d->num_q_heads / d->num_kv_heads > tts::kMaxRows)
     return fail(TTS_ERR_UNSUPPORTED, "more than 64 query heads per KV head");
   if (d->head_dim != 64 && d->head_dim != 128) return fail(TTS_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
   if (d->block_size != 16) return fail(TTS_ERR_UNSUPPORTED, "block_size must be 16");
@@ -79,9 +79,9 @@ struct tts_prefix_meta {
   tts_attn_desc desc{};
   tts::WorkPlan plan;
   int32_t num_blocks = 0;
-  // device buffer: perm | tail_lblock | slot_base | seg_blocks | units
+  // device buffer: unit records | slot table | build_len
   void* dev = nullptr;
-  size_t off_perm = 0, off_tail = 0, off_slot = 0, off_seg = 0, off_units = 0;
+  size_t off_recs = 0, off_slot_tab = 0, off_build = 0;
 };
 
 extern "C" {
@@ -126,28 +126,29 @@ tts_status tts_build_prefix_meta(int32_t num_reqs, const int32_t* req_seq_offset
   if (desc) {
     m->has_plan = true;
     m->desc = *desc;
+    int dev_id = 0, ncu = 0;
+    if (hipGetDevice(&dev_id) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev_id) != hipSuccess || ncu <= 0) {
+      delete m;
+      return fail(TTS_ERR_HIP, "cannot query the device's compute-unit count");
+    }
     try {
-      tts::build_work_plan(m->host, {desc->num_q_heads, desc->num_kv_heads, desc->head_dim, kv_bytes(desc)},
+      tts::build_work_plan(m->host, {desc->num_q_heads, desc->num_kv_heads, desc->head_dim, kv_bytes(desc), ncu},
                            &m->plan);
     } catch (const std::bad_alloc&) {
       delete m;
       return fail(TTS_ERR_NOMEM, "out of host memory");
     }
     const size_t S = static_cast<size_t>(num_seqs);
-    m->off_perm = 0;
-    m->off_tail = align256(m->off_perm + S * 4);
-    m->off_slot = align256(m->off_tail + S * 4);
-    m->off_seg = align256(m->off_slot + (S + 1) * 4);
-    m->off_units = align256(m->off_seg + m->plan.seg_blocks.size() * 4);
-    const size_t total = align256(m->off_units + m->plan.units.size() * sizeof(tts::Unit));
+    const auto& pl = m->plan;
+    m->off_recs = 0;
+    m->off_slot_tab = align256(m->off_recs + pl.recs.size() * sizeof(tts::UnitRec));
+    m->off_build = align256(m->off_slot_tab + pl.slot_tab.size() * 4);
+    const size_t total = align256(m->off_build + S * 4);
     std::vector<unsigned char> img(total, 0);
-    std::memcpy(img.data() + m->off_perm, m->host.perm.data(), S * 4);
-    std::memcpy(img.data() + m->off_tail, m->host.tail_lblock.data(), S * 4);
-    std::memcpy(img.data() + m->off_slot, m->plan.slot_base.data(), (S + 1) * 4);
-    if (!m->plan.seg_blocks.empty())
-      std::memcpy(img.data() + m->off_seg, m->plan.seg_blocks.data(), m->plan.seg_blocks.size() * 4);
-    if (!m->plan.units.empty())
-      std::memcpy(img.data() + m->off_units, m->plan.units.data(), m->plan.units.size() * sizeof(tts::Unit));
+    std::memcpy(img.data() + m->off_recs, pl.recs.data(), pl.recs.size() * sizeof(tts::UnitRec));
+    if (!pl.slot_tab.empty()) std::memcpy(img.data() + m->off_slot_tab, pl.slot_tab.data(), pl.slot_tab.size() * 4);
+    if (S) std::memcpy(img.data() + m->off_build, pl.build_len.data(), S * 4);
     hipError_t e = hipMalloc(&m->dev, total);
     if (e != hipSuccess) {
       m->dev = nullptr;
@@ -210,7 +211,7 @@ tts_status tts_prefix_meta_coverage(const tts_prefix_meta* m, const int32_t* seq
 tts_status tts_prefix_meta_stats(const tts_prefix_meta* m, int64_t* num_units, int64_t* num_slots) {
   if (!m || !num_units || !num_slots) return fail(TTS_ERR_INVALID_ARG, "NULL argument");
   if (!m->has_plan) return fail(TTS_ERR_INVALID_ARG, "metadata was built without a desc");
-  *num_units = static_cast<int64_t>(m->plan.units.size());
+  *num_units = m->plan.num_units;
   *num_slots = m->plan.num_slots;
   return ok();
 }
@@ -273,7 +274,7 @@ tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const
   p.paged_max_len = max_seq_len;
   const int64_t units = static_cast<int64_t>(num_seqs) * d->num_kv_heads * ns;
   if (units > 0x7FFFFFFF) return fail(TTS_ERR_UNSUPPORTED, "grid too large");
-  hipError_t e = tts::launch_attn_units(p, static_cast<int>(units), d->head_dim, kv_kind(d), stream);
+  hipError_t e = tts::launch_attn(p, static_cast<int>(units), d->head_dim, kv_kind(d), stream);
   if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("attention launch: ") + hipGetErrorString(e));
   if (ns > 1) {
     tts::MergeParams mp{};
@@ -283,6 +284,7 @@ tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const
     mp.out = p.out;
     mp.num_seqs = num_seqs;
     mp.hq = d->num_q_heads;
+    mp.g = d->num_q_heads / d->num_kv_heads;
     mp.paged_nsplit = ns;
     e = tts::launch_merge(mp, d->head_dim, stream);
     if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
@@ -292,7 +294,7 @@ tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const
 
 size_t tts_prefix_decode_workspace_size(const tts_attn_desc* d, const tts_prefix_meta* m) {
   if (!d || !m || !m->has_plan || check_desc(d) != TTS_OK) return 0;
-  const size_t rows = static_cast<size_t>(m->plan.num_slots) * d->num_q_heads;
+  const size_t rows = static_cast<size_t>(m->plan.rows_per_head) * d->num_kv_heads;
   return align256(rows * d->head_dim * 4) + align256(rows * 2 * 4);
 }
 
@@ -325,7 +327,7 @@ tts_status prefix_params(const tts_attn_desc* d, const tts_prefix_meta* m, const
   const size_t need = tts_prefix_decode_workspace_size(d, m);
   if (!workspace || workspace_bytes < need)
     return fail(TTS_ERR_WORKSPACE, "workspace smaller than tts_prefix_decode_workspace_size");
-  const size_t rows = static_cast<size_t>(m->plan.num_slots) * d->num_q_heads;
+  const size_t rows = static_cast<size_t>(m->plan.rows_per_head) * d->num_kv_heads;
   const char* dev = static_cast<const char*>(m->dev);
   *p = tts::AttnParams{};
   p->q = q;
@@ -338,11 +340,9 @@ tts_status prefix_params(const tts_attn_desc* d, const tts_prefix_meta* m, const
   p->out = static_cast<float*>(out);
   p->part_o = static_cast<float*>(workspace);
   p->part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * d->head_dim * 4));
-  p->perm = reinterpret_cast<const int32_t*>(dev + m->off_perm);
-  p->tail_lblock = reinterpret_cast<const int32_t*>(dev + m->off_tail);
-  p->slot_base = reinterpret_cast<const int32_t*>(dev + m->off_slot);
-  p->seg_blocks = reinterpret_cast<const int32_t*>(dev + m->off_seg);
-  p->units = reinterpret_cast<const tts::Unit*>(dev + m->off_units);
+  p->recs = reinterpret_cast<const tts::UnitRec*>(dev + m->off_recs);
+  p->build_len = reinterpret_cast<const int32_t*>(dev + m->off_build);
+  p->rows_per_head = m->plan.rows_per_head;
   p->max_blocks = max_blocks_per_seq;
   p->num_blocks = num_blocks;
   p->num_seqs = S;
@@ -355,22 +355,26 @@ tts_status prefix_params(const tts_attn_desc* d, const tts_prefix_meta* m, const
 
 tts_status launch_partials(const tts_attn_desc* d, const tts_prefix_meta* m, const tts::AttnParams& p,
                            hipStream_t stream) {
-  hipError_t e =
-      tts::launch_attn_units(p, static_cast<int>(m->plan.units.size()), d->head_dim, kv_kind(d), stream);
+  hipError_t e = tts::launch_attn(p, m->plan.num_bins, d->head_dim, kv_kind(d), stream);
   if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("attention launch: ") + hipGetErrorString(e));
   return TTS_OK;
 }
 
-tts_status launch_prefix_merge(const tts_attn_desc* d, const tts::AttnParams& p, hipStream_t stream) {
+tts_status launch_prefix_merge(const tts_attn_desc* d, const tts_prefix_meta* m, const tts::AttnParams& p,
+                               hipStream_t stream) {
+  const char* dev = static_cast<const char*>(m->dev);
   tts::MergeParams mp{};
   mp.part_o = p.part_o;
   mp.part_ml = p.part_ml;
-  mp.slot_base = p.slot_base;
+  mp.slot_tab = reinterpret_cast<const int32_t*>(dev + m->off_slot_tab);
+  mp.slot_stride = m->plan.slot_stride;
   mp.seq_lens = p.seq_lens;
-  mp.tail_lblock = p.tail_lblock;
+  mp.build_len = p.build_len;
   mp.out = p.out;
   mp.num_seqs = p.num_seqs;
   mp.hq = d->num_q_heads;
+  mp.g = p.g;
+  mp.rows_per_head = p.rows_per_head;
   hipError_t e = tts::launch_merge(mp, d->head_dim, stream);
   if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
   return TTS_OK;
@@ -388,7 +392,7 @@ tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta*
                                seq_lens, num_blocks, out, workspace, workspace_bytes, true, &p);
   if (s != TTS_OK || m->host.num_seqs == 0) return s == TTS_OK ? ok() : s;
   if ((s = launch_partials(d, m, p, stream)) != TTS_OK) return s;
-  if ((s = launch_prefix_merge(d, p, stream)) != TTS_OK) return s;
+  if ((s = launch_prefix_merge(d, m, p, stream)) != TTS_OK) return s;
   return ok();
 }
 
@@ -411,15 +415,15 @@ tts_status tts_prefix_decode_merge(const tts_attn_desc* d, const tts_prefix_meta
   tts_status s = prefix_params(d, m, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0, seq_lens, 0, out,
                                workspace, workspace_bytes, false, &p);
   if (s != TTS_OK || m->host.num_seqs == 0) return s == TTS_OK ? ok() : s;
-  if ((s = launch_prefix_merge(d, p, stream)) != TTS_OK) return s;
+  if ((s = launch_prefix_merge(d, m, p, stream)) != TTS_OK) return s;
   return ok();
 }
 
 #ifdef TTS_PROFILE_UNITS
-// Tuning builds only: copy the work list of a handle (12 int32 per unit).
-int64_t tts_prof_units(const tts_prefix_meta* m, int32_t* out, int64_t cap) {
-  const int64_t n = static_cast<int64_t>(m->plan.units.size());
-  if (out) std::memcpy(out, m->plan.units.data(), sizeof(tts::Unit) * static_cast<size_t>(std::min(n, cap)));
+// Tuning builds only: copy the unit records of a handle.
+int64_t tts_prof_recs(const tts_prefix_meta* m, void* out, int64_t cap) {
+  const int64_t n = static_cast<int64_t>(m->plan.recs.size());
+  if (out) std::memcpy(out, m->plan.recs.data(), sizeof(tts::UnitRec) * static_cast<size_t>(std::min(n, cap)));
   return n;
 }
 #endif

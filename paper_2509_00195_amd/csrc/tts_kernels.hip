@@ -1,31 +1,38 @@
 // HIP kernels (gfx950) for prefix-shared beam decode attention.
 //
-// One kernel processes "work units" (tts_work.h): the query rows of up to
-// 64 / g whole beams for one KV head against a run of KV blocks.
+// attn_kernel: one workgroup (4 waves) per compute unit walks a chain of
+// work units (tts_work.h). A unit holds up to 64 query rows of one KV head
+// -- whole beams, 4 row tiles of 16 -- and up to 64 KV blocks, each applying
+// to a contiguous range of the rows. Every wave keeps the softmax state of
+// ALL of the unit's rows in registers and streams its own share of the
+// unit's block pairs (pairs w, w + 4, ...) straight from HBM into registers,
+// one pair ahead of the one it computes; no LDS staging, no barriers until
+// the four waves combine their states at the end of the unit.
 //
-// Products on MFMA, two 16-token blocks ("a pair") at a time:
-//   S^T = K Q^T   : 2 x v_mfma_f32_16x16x32_bf16 per 32-dim slice
-//                   (M = 16 tokens, N = 16 query rows, K = head dim)
-//   O^T += V^T P^T: 1 x v_mfma_f32_16x16x32_bf16 per 16 output dims
-//                   (M = 16 dims, N = 16 rows, K = the pair's 32 tokens)
+// Products on MFMA, two 16-token blocks ("a pair") at a time, per row tile:
+//   S^T = K Q^T   : 2 x 4 v_mfma_f32_16x16x32_bf16 (M = 16 tokens, N = 16
+//                   rows, K = 128 head dims)
+//   O^T += V^T P^T: 8 x v_mfma_f32_16x16x32_bf16 (M = 16 dims, N = 16 rows,
+//                   K = the pair's 32 tokens)
 // The two S tiles of a pair take their 16 token rows in an interleaved
 // order (tile t, row m -> token 8*(m/4) + 4*t + m%4), so after the first
-// product every lane holds the scores of 8 consecutive tokens of one row:
-// exactly the B operand the second product needs, with no data movement.
-// Values are stored dim-major inside a block, so the matching A operand is
-// one contiguous 16-byte read.
+// product every lane holds the scores of 8 consecutive tokens of one row,
+// all in one block of the pair: exactly the B operand of the second
+// product. Values are stored dim-major inside a block, so the matching A
+// operand is one contiguous 16-byte read.
 //
-// Softmax is online with a lazy reference maximum: probabilities are
-// exp2(s - m_ref) and O/l are rescaled only when some score exceeds m_ref
-// by more than kRescale (a wave vote decides), which keeps the common path
-// free of cross-lane reductions and accumulator rescaling.
+// Softmax without a running maximum: probabilities are exp2(s - m_ref) with
+// a fixed reference m_ref = 0 (log2 units), so the hot loop has no
+// cross-lane reductions, no accumulator rescaling and no data-dependent
+// branches. Each lane tracks the largest score it has seen; if a row's
+// maximum leaves [-kRefWindow, kRefWindow] (where exp2 could overflow the
+// fp32 accumulators or underflow every weight), the wave recomputes its
+// pairs with m_ref = that row's exact maximum. Either way each row ends
+// with a consistent (m_ref, l, o) triple.
 //
-// Units with more than 16 rows stage each chunk of K/V blocks in LDS once
-// and every wave (16 rows each) reads it; units with at most 16 rows (a
-// private tail, a two-beam segment) let each wave stream its own block
-// pairs straight into registers. Partial softmax states go to the
-// workspace, and a second kernel merges each (beam, query head)'s partial
-// states in a fixed order (deterministic).
+// Every unit writes one partial softmax state (m, l, unnormalised o) per
+// row; merge_kernel combines each (beam, query head)'s states in a fixed
+// order (deterministic, no float atomics).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -36,14 +43,15 @@
 namespace tts {
 
 #ifdef TTS_PROFILE_UNITS
-// Per-unit timestamps for tuning builds only: start, end of the block loop,
-// end, and the XCC / HW_ID registers of the workgroup.
-constexpr int kProfSlots = 1 << 16;
-__device__ uint64_t g_prof[kProfSlots][4];
-#define TTS_PROF_MARK(k) \
-  do { if (threadIdx.x == 0 && blockIdx.x < kProfSlots) g_prof[blockIdx.x][k] = wall_clock64(); } while (0)
+// Per-unit timestamps for tuning builds only (indexed by record): start,
+// end of wave 0's block loop, end, the XCC / HW_ID registers, all waves
+// done, next unit issued, combine area written.
+constexpr int kProfSlots = 1 << 15;
+__device__ uint64_t g_prof[kProfSlots][8];
+#define TTS_PROF_MARK(k, i) \
+  do { if (threadIdx.x == 0 && (i) < kProfSlots) g_prof[(i)][k] = wall_clock64(); } while (0)
 #else
-#define TTS_PROF_MARK(k) do {} while (0)
+#define TTS_PROF_MARK(k, i) do {} while (0)
 #endif
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -54,8 +62,10 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 constexpr int kTok = 16;  // tokens per KV block
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
+constexpr int kTiles = kMaxRows / 16;
+constexpr int kWideTiles = kMaxWideRows / 16 / 4;  // row tiles per wave in a wide unit
 constexpr float kNegInf = -__builtin_inff();
-constexpr float kRescale = 8.0f;  // log2 headroom before O and l are rescaled
+constexpr float kRefWindow = 64.0f;  // |row max| (log2 units) handled with m_ref = 0
 
 enum KvKind : int { kKvF32 = 0, kKvBf16 = 1, kKvFp8 = 2 };
 
@@ -67,20 +77,13 @@ struct KvBytes {
 template <int D, int KV>
 struct Geo {
   static constexpr int eb = KvBytes<KV>::value;
-  static constexpr int row_bytes = D * eb;            // one token of K
-  static constexpr int c16 = row_bytes / 16;           // 16-byte columns per K row
-  static constexpr int blk_bytes = kTok * row_bytes;   // one (block, head) of K or V
-  static constexpr int vrow_bytes = kTok * eb;         // one dim of V (16 tokens)
-  // LDS stages of one block pair (K0, V0, K1, V1) for the staged path:
-  // four when a stage is at most 16 KB, else two.
-  static constexpr int stage_bytes = 4 * blk_bytes;
-  static constexpr int stages = stage_bytes <= 16384 ? 4 : 2;
-  static constexpr int dma_per_wave = blk_bytes / 1024;  // 1-KB wave loads per tensor
-  // Per-wave softmax state exchanged at the end: 16 rows of D floats padded
-  // by 4 (bank spread) plus m and l; it reuses a stage.
-  static constexpr int combine_bytes = (kTok * (D + 4) + 2 * kTok) * 4;
-  static constexpr int stage_alloc = stage_bytes > combine_bytes ? stage_bytes : combine_bytes;
-  static_assert(blk_bytes % 1024 == 0, "whole 1-KB wave loads");
+  static constexpr int row_bytes = D * eb;           // one token of K
+  static constexpr int blk_bytes = kTok * row_bytes;  // one (block, head) of K or V
+  static constexpr int vrow_bytes = kTok * eb;        // one dim of V (16 tokens)
+  // End-of-unit combine: per (wave, tile) 16 rows of D floats padded by 4
+  // (bank spread), then m and l.
+  static constexpr int comb_row = D + 4;
+  static constexpr int comb_floats = kTok * comb_row + 2 * kTok;
 };
 
 __device__ __forceinline__ uint32_t f32_bits(float x) { return __builtin_bit_cast(uint32_t, x); }
@@ -112,38 +115,168 @@ __device__ __forceinline__ float xlane_sum16(float x) {
   return x + __shfl_xor(x, 32);
 }
 
-// Per-lane operands of one block pair: K fragments of the two S tiles and
-// V^T fragments of every 16-dim slice (bf16 compute: bf16 bits; f32
-// compute: raw floats).
+__device__ __forceinline__ int rl(int x, int i) { return __builtin_amdgcn_readlane(x, i); }
+__device__ __forceinline__ float rlf(float x, int i) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), i));
+}
+
+// Token row of S tile t, MFMA row m inside a pair (see the header).
+__device__ __forceinline__ int pair_token(int t, int m) { return ((m >> 2) << 3) + (t << 2) + (m & 3); }
+
+// Operands of one block pair in compute form: bf16 bits (bf16 and fp8
+// caches) or fp32. Lane (ln, lq):
+//   k[t][j]: K of token pair_token(t, ln), dims 32j + 8lq .. + 8 (bf16)
+//            or 16j + 4lq .. + 4 (fp32);
+//   v[dt]  : V of dim 16dt + ln, tokens 8lq .. 8lq + 7 of the pair.
 template <int D, int KV>
-struct PairFrags {
+struct Ops {
   static constexpr bool f32 = KV == kKvF32;
-  static constexpr int kk = f32 ? D / 16 : D / 32;  // K-fragment slices per tile
-  typedef typename std::conditional<f32, f32x4, uint4>::type KF;
-  KF k[2][kk];
-  // V^T: lane (d = 16*dt + ln, tokens 8*lq .. 8*lq+7)
-  typedef typename std::conditional<f32, f32x4, uint4>::type VF;
-  VF v[D / 16][f32 ? 2 : 1];
+  static constexpr int kk = f32 ? D / 16 : D / 32;
+  typedef typename std::conditional<f32, f32x4, uint4>::type T;
+  T k[2][kk];
+  T v[D / 16][f32 ? 2 : 1];
 };
 
-// Softmax state of one wave's 16 rows (lane ln = row, lq = token group).
+// fp8 caches load raw codes (half the registers) and convert per pair.
+template <int D>
+struct Fp8Frags {
+  static constexpr int kk = D / 32;
+  typedef uint2 T;
+  uint2 k[2][kk];
+  uint2 v[D / 16][1];
+};
+
+template <int D, int KV>
+using Frags = typename std::conditional<KV == kKvFp8, Fp8Frags<D>, Ops<D, KV>>::type;
+
+// standin: every load reads the first bytes of kb0 instead (a placeholder
+// whose data is never used).
+template <int D, int KV>
+__device__ __forceinline__ void load_pair(Frags<D, KV>& f, const unsigned char* kb0, const unsigned char* kb1,
+                                          const unsigned char* vb0, const unsigned char* vb1, int ln, int lq,
+                                          bool standin = false) {
+  using G = Geo<D, KV>;
+  using F = Frags<D, KV>;
+  typedef typename F::T T;
+  auto at = [&](const unsigned char* a) { return reinterpret_cast<const T*>(standin ? kb0 : a); };
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int tok = pair_token(t, ln);
+    const unsigned char* kr = (tok < 16 ? kb0 : kb1) + (tok & 15) * G::row_bytes;
+#pragma unroll
+    for (int j = 0; j < F::kk; ++j) {
+      if constexpr (KV == kKvFp8)
+        f.k[t][j] = *at(kr + 32 * j + 8 * lq);
+      else
+        f.k[t][j] = *at(kr + (4 * j + lq) * 16);
+    }
+  }
+  const unsigned char* vb = (lq >= 2 ? vb1 : vb0) + (lq & 1) * 8 * G::eb + ln * G::vrow_bytes;
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt) {
+    const unsigned char* vr = vb + 16 * dt * G::vrow_bytes;
+    f.v[dt][0] = *at(vr);
+    if constexpr (KV == kKvF32) f.v[dt][1] = *at(vr + 16);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void fp8_to_ops(const Fp8Frags<D>& f, Ops<D, kKvFp8>& o) {
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int j = 0; j < D / 32; ++j) o.k[t][j] = fp8x8_to_bf16x8(f.k[t][j]);
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt) o.v[dt][0] = fp8x8_to_bf16x8(f.v[dt][0]);
+}
+
+// Zero the V^T operands of tokens past `valid` in this lane's block, so
+// unused slots of a partial block never reach the value product.
+template <int D, int KV>
+__device__ __forceinline__ void mask_v(Ops<D, KV>& o, int lq, int valid0, int valid1) {
+  const int valid = lq >= 2 ? valid1 : valid0;
+  const int slot0 = 8 * (lq & 1);
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt) {
+    if constexpr (KV == kKvF32) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (slot0 + 4 * h + e >= valid) o.v[dt][h][e] = 0.f;
+    } else {
+      uint32_t* a = reinterpret_cast<uint32_t*>(&o.v[dt][0]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t keep =
+            (slot0 + 2 * e < valid ? 0x0000FFFFu : 0u) | (slot0 + 2 * e + 1 < valid ? 0xFFFF0000u : 0u);
+        a[e] &= keep;
+      }
+    }
+  }
+}
+
+// Query rows of the unit in LDS (B operand of S^T = K Q^T): row r is D
+// elements (bf16, or fp32 for fp32 caches), its 16-byte columns XOR-swizzled
+// by the row so that the 16 lanes of a column read distinct banks.
+template <int D, int KV>
+struct QLds {
+  static constexpr int eb = KV == kKvF32 ? 4 : 2;
+  static constexpr int row_bytes = D * eb;
+  static constexpr int ncol = row_bytes / 16;
+  static constexpr int swz_mask = (ncol < 16 ? ncol : 16) - 1;
+  static constexpr int bytes = kMaxRows * row_bytes;
+  static __device__ __forceinline__ int offset(int row, int col) {
+    return row * row_bytes + ((col ^ (row & swz_mask)) << 4);
+  }
+};
+
+// Softmax state of one row tile (lane ln = row, lq = token / dim group).
 template <int D>
 struct RowState {
   f32x4 o[D / 16];
-  float m;  // reference max (log2 units), uniform over the 4 lanes of a row
-  float l;  // per-lane partial sum
+  float m;     // reference (log2 units), uniform over the 4 lanes of a row
+  float l;     // per-lane partial sum
+  float seen;  // largest scaled score this lane has seen (-inf: none)
+};
+
+// Uniform description of one pair: blocks' valid tokens, row ranges and
+// (fp8) scales.
+struct PairInfo {
+  int v0, v1;      // valid tokens (0: no block)
+  int a0, e0;      // rows [a0, e0) of block 0
+  int a1, e1;      // rows [a1, e1) of block 1
+  float ks0, ks1;  // logit scale (softmax scale * log2 e * k_scale)
+  float vs0, vs1;  // value scale (fp8) or 1
+};
+
+// One pair against one row tile `r`.
+// Query operands of one row tile (lane: row 16r + ln, dims as K's).
+template <int D, int KV>
+struct QFrag {
+  typename Ops<D, KV>::T q[Ops<D, KV>::kk];
 };
 
 template <int D, int KV>
-__device__ __forceinline__ void pair_step(const PairFrags<D, KV>& f, const void* qf_, RowState<D>& st, int lq,
-                                          float sc0, float sc1, float vs0, float vs1, int valid0, int valid1,
-                                          bool masked) {
-  using F = PairFrags<D, KV>;
-  f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-  if constexpr (F::f32) {
-    const f32x4* qf = static_cast<const f32x4*>(qf_);
+__device__ __forceinline__ QFrag<D, KV> q_from_lds(const unsigned char* qlds, int r, int ln, int lq) {
+  using O = Ops<D, KV>;
+  using Q = QLds<D, KV>;
+  QFrag<D, KV> qf;
 #pragma unroll
-    for (int j = 0; j < F::kk; ++j) {
+  for (int j = 0; j < O::kk; ++j)
+    qf.q[j] = *reinterpret_cast<const typename O::T*>(qlds + Q::offset(16 * r + ln, 4 * j + lq));
+  return qf;
+}
+
+template <int D, int KV>
+__device__ __forceinline__ void tile_step(const Ops<D, KV>& f, const QFrag<D, KV>& qfr, RowState<D>& st,
+                                          const PairInfo& pi, int r, int ln, int lq) {
+  using O = Ops<D, KV>;
+  const auto& qf = qfr.q;
+  f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  if constexpr (O::f32) {
+#pragma unroll
+    for (int j = 0; j < O::kk; ++j)
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.k[t][j].x, qf[j].x, acc[t], 0, 0, 0);
@@ -151,58 +284,48 @@ __device__ __forceinline__ void pair_step(const PairFrags<D, KV>& f, const void*
         acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.k[t][j].z, qf[j].z, acc[t], 0, 0, 0);
         acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.k[t][j].w, qf[j].w, acc[t], 0, 0, 0);
       }
-    }
   } else {
-    const uint4* qf = static_cast<const uint4*>(qf_);
 #pragma unroll
-    for (int j = 0; j < F::kk; ++j) {
+    for (int j = 0; j < O::kk; ++j)
 #pragma unroll
       for (int t = 0; t < 2; ++t)
         acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, f.k[t][j]),
                                                          __builtin_bit_cast(bf16x8, qf[j]), acc[t], 0, 0, 0);
-    }
   }
-  // Lane (ln, lq) holds row ln, tokens 8*lq + 4*t + i of the pair; they all
-  // lie in block lq >> 1 of the pair, at slots 8*(lq & 1) + 4*t + i.
-  // bf16/fp32 scores stay unscaled (their scale is positive, so it
-  // preserves the maximum) and the scale is applied inside the exponent:
-  // p = 2^(acc * sc - m).
+  // Lane (ln, lq) holds row 16r + ln, tokens 8lq + 4t + i of the pair: all in
+  // block lq >> 1, at slots 8(lq & 1) + 4t + i.
   const bool hi = lq >= 2;
-  const float sc = hi ? sc1 : sc0;
-  // fp8 block scales are caller data (any sign): scale first there.
+  const float sc = hi ? pi.ks1 : pi.ks0;
+  // fp8 block scales are caller data (any sign): scale first there. For the
+  // others the positive scale preserves the maximum and goes into exp2.
   constexpr bool kPreScale = KV == kKvFp8;
   float s[8];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) s[4 * t + i] = kPreScale ? acc[t][i] * sc : acc[t][i];
-  if (masked) {
-    const int valid = hi ? valid1 : valid0;
+  const int row = 16 * r + ln;
+  const int valid = hi ? pi.v1 : pi.v0;
+  const int ra = hi ? pi.a1 : pi.a0, re = hi ? pi.e1 : pi.e0;
+  const bool full = pi.v0 == kTok && pi.v1 == kTok && pi.a0 <= 16 * r && pi.e0 >= 16 * r + 16 &&
+                    pi.a1 <= 16 * r && pi.e1 >= 16 * r + 16;
+  if (!full) {
+    const int lim = (row >= ra && row < re) ? valid : 0;
     const int slot0 = 8 * (lq & 1);
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        if (slot0 + 4 * t + i >= valid) s[4 * t + i] = kNegInf;
+        if (slot0 + 4 * t + i >= lim) s[4 * t + i] = kNegInf;
   }
   float smax = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
-  const float lm = kPreScale ? smax : smax * sc;  // largest scaled score of this lane (-inf if all masked)
-  if (__builtin_amdgcn_ballot_w64(lm > st.m + kRescale) != 0) {
-    // Rare: move the reference maximum up for every row of the wave.
-    const float rmax = xlane_max16(lm);
-    const float m_new = fmaxf(st.m, rmax);
-    const float alpha = (st.m == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(st.m - m_new);
-    st.l *= alpha;
-#pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) st.o[dt] *= alpha;
-    st.m = m_new;
-  }
-  const float mu = (st.m == kNegInf) ? 0.f : st.m;
+  st.seen = fmaxf(st.seen, kPreScale ? smax : smax * sc);
   float p[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) p[i] = __builtin_amdgcn_exp2f(kPreScale ? s[i] - mu : __builtin_fmaf(s[i], sc, -mu));
+  for (int i = 0; i < 8; ++i)
+    p[i] = __builtin_amdgcn_exp2f(kPreScale ? s[i] - st.m : __builtin_fmaf(s[i], sc, -st.m));
   st.l += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
-  if constexpr (F::f32) {
+  if constexpr (O::f32) {
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) {
       const f32x4 a0 = f.v[dt][0], a1 = f.v[dt][1];
@@ -218,9 +341,10 @@ __device__ __forceinline__ void pair_step(const PairFrags<D, KV>& f, const void*
       st.o[dt] = o;
     }
   } else {
+    const float vs = hi ? pi.vs1 : pi.vs0;
     float pv[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) pv[i] = (KV == kKvFp8) ? p[i] * (hi ? vs1 : vs0) : p[i];
+    for (int i = 0; i < 8; ++i) pv[i] = (KV == kKvFp8) ? p[i] * vs : p[i];
     const uint4 pb = {pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]), pack_bf16x2(pv[4], pv[5]),
                       pack_bf16x2(pv[6], pv[7])};
     const bf16x8 pbf = __builtin_bit_cast(bf16x8, pb);
@@ -231,614 +355,780 @@ __device__ __forceinline__ void pair_step(const PairFrags<D, KV>& f, const void*
   }
 }
 
-// LDS swizzles of the staged path (bank-conflict-free fragment reads).
-// K: an S tile reads rows {0-3, 8-11} or {4-7, 12-15} of both blocks of a
-// pair, so the 16-byte column of (block b, row r) is XORed with
-// (r & 3) | ((r >> 3) & 1) << 2 | b << 3 (cut to the columns a row has).
-// V^T: lanes read 16 consecutive dims at a 32-byte stride; the two 16-byte
-// halves of a dim row swap on odd groups of 8 dims.
-template <int C16>
-__device__ __forceinline__ int k_swz(int b, int r) {
-  return ((r & 3) | (((r >> 3) & 1) << 2) | (b << 3)) & (C16 - 1);
-}
-__device__ __forceinline__ int v_half_swz(int d) { return (d >> 3) & 1; }
-
-// Token row of S tile t, MFMA row m inside a pair (see the header).
-__device__ __forceinline__ int pair_token(int t, int m) { return ((m >> 2) << 3) + (t << 2) + (m & 3); }
-
-// K fragments of one pair straight from global memory.
+// ---- wide units: block pairs shared by the four waves through LDS --------
+// A pair's operands are kChunks 16-byte fragments per lane (K: tile t, slice
+// j; then V: dim tile dt). Each wave loads a quarter of them (the
+// fragments of all 64 lanes, from the addresses load_pair reads) into
+// registers one pair ahead, stores them to an LDS stage -- chunk c holds
+// fragment c of every lane, lane i at byte 16 i -- and after a barrier every
+// wave reads all chunks. (Plain loads stream faster than global-to-LDS
+// copies here.)
 template <int D, int KV>
-__device__ __forceinline__ void load_k_global(PairFrags<D, KV>& f, const unsigned char* kb0,
-                                              const unsigned char* kb1, int ln, int lq) {
-  using G = Geo<D, KV>;
-#pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int tok = pair_token(t, ln);
-    const unsigned char* kr = (tok < 16 ? kb0 : kb1) + (tok & 15) * G::row_bytes;
-#pragma unroll
-    for (int j = 0; j < PairFrags<D, KV>::kk; ++j) {
-      if constexpr (KV == kKvF32) {
-        f.k[t][j] = *reinterpret_cast<const f32x4*>(kr + (4 * j + lq) * 16);
-      } else if constexpr (KV == kKvBf16) {
-        f.k[t][j] = *reinterpret_cast<const uint4*>(kr + (4 * j + lq) * 16);
-      } else {
-        f.k[t][j] = fp8x8_to_bf16x8(*reinterpret_cast<const uint2*>(kr + 32 * j + 8 * lq));
-      }
-    }
-  }
-}
-
-// V^T fragments of one pair (lane: dim 16*dt + ln, tokens 8*lq .. 8*lq+7)
-// from two blocks laid out dim-major; works for global memory and LDS.
-template <int D, int KV>
-__device__ __forceinline__ void load_v(PairFrags<D, KV>& f, const unsigned char* vb0, const unsigned char* vb1, int ln,
-                                       int lq) {
-  using G = Geo<D, KV>;
-  const unsigned char* vb = (lq >= 2 ? vb1 : vb0) + (lq & 1) * 8 * G::eb + ln * G::vrow_bytes;
-#pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) {
-    const unsigned char* vr = vb + 16 * dt * G::vrow_bytes;
-    if constexpr (KV == kKvF32) {
-      f.v[dt][0] = *reinterpret_cast<const f32x4*>(vr);
-      f.v[dt][1] = *reinterpret_cast<const f32x4*>(vr + 16);
-    } else if constexpr (KV == kKvBf16) {
-      f.v[dt][0] = *reinterpret_cast<const uint4*>(vr);
-    } else {
-      f.v[dt][0] = fp8x8_to_bf16x8(*reinterpret_cast<const uint2*>(vr));
-    }
-  }
-}
-
-// LDS fragment reads of the staged path are written as inline asm: the
-// compiler's wait insertion cannot tell which stage an in-flight
-// global-to-LDS copy targets once the read sits behind a branch, and would
-// otherwise drain every copy before each read. lds_ready() then waits for
-// this wave's LDS reads and ties each value to that wait, so no use can be
-// scheduled before it.
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) void*)(p)));
-}
-__device__ __forceinline__ u32x4 lds_rd128(const unsigned char* p) {
-  u32x4 v;
-  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(lds_addr(p)) : "memory");
-  return v;
-}
-__device__ __forceinline__ u32x2 lds_rd64(const unsigned char* p) {
-  u32x2 v;
-  asm volatile("ds_read_b64 %0, %1" : "=v"(v) : "v"(lds_addr(p)) : "memory");
-  return v;
-}
-__device__ __forceinline__ void lds_wait_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-template <typename T>
-__device__ __forceinline__ void lds_tie(T& v) { asm volatile("" : "+v"(v)); }
-
-// V^T fragments of one pair from an LDS stage (bf16: halves swizzled).
-// K and V^T fragments of one pair from an LDS stage (K rows XOR-swizzled,
-// bf16 V^T halves swizzled; see k_swz / v_half_swz).
-template <int D, int KV>
-__device__ __forceinline__ void load_pair_lds(PairFrags<D, KV>& f, const unsigned char* k0, const unsigned char* k1,
-                                              const unsigned char* v0, const unsigned char* v1, int ln, int lq) {
-  using G = Geo<D, KV>;
-  constexpr int kk = PairFrags<D, KV>::kk;
-  constexpr bool wide = KV != kKvFp8;  // 16-byte reads (fp8: 8 bytes)
-  typedef typename std::conditional<wide, u32x4, u32x2>::type R;
-  R rk[2][kk];
-  R rv[D / 16][KV == kKvF32 ? 2 : 1];
-#pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int tok = pair_token(t, ln);
-    const int r = tok & 15;
-    const unsigned char* kr = (tok < 16 ? k0 : k1) + r * G::row_bytes;
-    const int sw = k_swz<G::c16>(tok >> 4, r);
-#pragma unroll
-    for (int j = 0; j < kk; ++j) {
-      if constexpr (wide) {
-        rk[t][j] = lds_rd128(kr + (((4 * j + lq) ^ sw) << 4));
-      } else {
-        const int col = 2 * j + (lq >> 1);
-        rk[t][j] = lds_rd64(kr + ((col ^ sw) << 4) + 8 * (lq & 1));
-      }
-    }
-  }
-  const unsigned char* vb = lq >= 2 ? v1 : v0;
-#pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) {
-    const int d = 16 * dt + ln;
-    if constexpr (KV == kKvBf16) {
-      rv[dt][0] = lds_rd128(vb + d * G::vrow_bytes + 16 * ((lq & 1) ^ v_half_swz(d)));
-    } else if constexpr (KV == kKvF32) {
-      const unsigned char* vr = vb + d * G::vrow_bytes + (lq & 1) * 32;
-      rv[dt][0] = lds_rd128(vr);
-      rv[dt][1] = lds_rd128(vr + 16);
-    } else {
-      rv[dt][0] = lds_rd64(vb + d * G::vrow_bytes + (lq & 1) * 8);
-    }
-  }
-  lds_wait_all();
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int j = 0; j < kk; ++j) lds_tie(rk[t][j]);
-#pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt)
-#pragma unroll
-    for (int h = 0; h < (KV == kKvF32 ? 2 : 1); ++h) lds_tie(rv[dt][h]);
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int j = 0; j < kk; ++j) {
-      if constexpr (KV == kKvF32) {
-        f.k[t][j] = __builtin_bit_cast(f32x4, rk[t][j]);
-      } else if constexpr (KV == kKvBf16) {
-        f.k[t][j] = __builtin_bit_cast(uint4, rk[t][j]);
-      } else {
-        f.k[t][j] = fp8x8_to_bf16x8(__builtin_bit_cast(uint2, rk[t][j]));
-      }
-    }
-#pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) {
-    if constexpr (KV == kKvF32) {
-      f.v[dt][0] = __builtin_bit_cast(f32x4, rv[dt][0]);
-      f.v[dt][1] = __builtin_bit_cast(f32x4, rv[dt][1]);
-    } else if constexpr (KV == kKvBf16) {
-      f.v[dt][0] = __builtin_bit_cast(uint4, rv[dt][0]);
-    } else {
-      f.v[dt][0] = fp8x8_to_bf16x8(__builtin_bit_cast(uint2, rv[dt][0]));
-    }
-  }
-}
-
-// Zero the V^T fragments of tokens past `valid` in this lane's block, so
-// unused slots of a partial block never reach the value product.
-template <int D, int KV>
-__device__ __forceinline__ void mask_v(PairFrags<D, KV>& f, int lq, int valid0, int valid1) {
-  const int valid = lq >= 2 ? valid1 : valid0;
-  const int slot0 = 8 * (lq & 1);
-#pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) {
-    if constexpr (KV == kKvF32) {
-      float* a = reinterpret_cast<float*>(&f.v[dt][0]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (slot0 + e >= valid) a[e] = 0.f;
-    } else {
-      uint32_t* a = reinterpret_cast<uint32_t*>(&f.v[dt][0]);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t keep =
-            (slot0 + 2 * e < valid ? 0x0000FFFFu : 0u) | (slot0 + 2 * e + 1 < valid ? 0xFFFF0000u : 0u);
-        a[e] &= keep;
-      }
-    }
-  }
-}
-
-// Block run of one unit, resolved from the metadata or the live tables.
-struct Run {
-  const int32_t* ids;  // block ids (segment) or table row (tail)
-  int32_t first;       // first index into ids
-  int32_t nblk;        // blocks in this unit
-  int32_t len;         // tail: beam length (last block may be partial)
-  bool tail;
+struct Stage {  // meaningful for bf16 caches (the only ones with wide units)
+  static constexpr int kKChunks = 2 * (D / 32);
+  static constexpr int kChunks = kKChunks + D / 16;
+  static constexpr int kPerWave = kChunks / kWaves;
+  static constexpr int bytes = kChunks * 1024;
+  static_assert(kChunks % kWaves == 0, "whole chunks per wave");
 };
 
-// Per-lane view of up to 64 consecutive blocks of a run: lane i holds the
-// id, valid token count and (fp8) scales of block w0 + i; a wave reads any
-// of them with a uniform index. Bad ids become valid = 0.
+template <int D, int KV>
+__device__ __forceinline__ const unsigned char* frag_src(int c, const unsigned char* kb0, const unsigned char* kb1,
+                                                         const unsigned char* vb0, const unsigned char* vb1, int ln,
+                                                         int lq) {
+  using G = Geo<D, KV>;
+  using S = Stage<D, KV>;
+  if (c < S::kKChunks) {
+    const int t = c / (D / 32), j = c % (D / 32);
+    const int tok = pair_token(t, ln);
+    return (tok < 16 ? kb0 : kb1) + (tok & 15) * G::row_bytes + (4 * j + lq) * 16;
+  }
+  const int dt = c - S::kKChunks;
+  return (lq >= 2 ? vb1 : vb0) + (lq & 1) * 8 * G::eb + ln * G::vrow_bytes + 16 * dt * G::vrow_bytes;
+}
+
+// (A vector value rather than an array, so that it stays in registers.)
+template <int D, int KV>
+struct Quarter {
+  typedef unsigned int V __attribute__((ext_vector_type(4 * Stage<D, KV>::kPerWave)));
+  V v;
+};
+
+// This wave's quarter of pair (id0, id1).
+template <int D, int KV>
+__device__ __forceinline__ void load_quarter(Quarter<D, KV>& q, int id0, int id1, const unsigned char* kbase,
+                                             const unsigned char* vbase, size_t blk_stride, int wave, int ln, int lq) {
+  using S = Stage<D, KV>;
+  const unsigned char* kb0 = kbase + id0 * blk_stride;
+  const unsigned char* kb1 = kbase + id1 * blk_stride;
+  const unsigned char* vb0 = vbase + id0 * blk_stride;
+  const unsigned char* vb1 = vbase + id1 * blk_stride;
+#pragma unroll
+  for (int i = 0; i < S::kPerWave; ++i) {
+    const uint4 t = *reinterpret_cast<const uint4*>(frag_src<D, KV>(wave + kWaves * i, kb0, kb1, vb0, vb1, ln, lq));
+    q.v[4 * i] = t.x;
+    q.v[4 * i + 1] = t.y;
+    q.v[4 * i + 2] = t.z;
+    q.v[4 * i + 3] = t.w;
+  }
+}
+
+template <int D, int KV>
+__device__ __forceinline__ void store_quarter(const Quarter<D, KV>& q, unsigned char* stage, int wave, int lane) {
+#pragma unroll
+  for (int i = 0; i < Stage<D, KV>::kPerWave; ++i)
+    *reinterpret_cast<uint4*>(stage + (wave + kWaves * i) * 1024 + lane * 16) =
+        uint4{q.v[4 * i], q.v[4 * i + 1], q.v[4 * i + 2], q.v[4 * i + 3]};
+}
+
+template <int D, int KV>
+__device__ __forceinline__ void read_stage(Ops<D, KV>& o, const unsigned char* stage, int lane) {
+  using S = Stage<D, KV>;
+#pragma unroll
+  for (int c = 0; c < S::kKChunks; ++c)
+    o.k[c / (D / 32)][c % (D / 32)] = *reinterpret_cast<const uint4*>(stage + c * 1024 + lane * 16);
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt)
+    o.v[dt][0] = *reinterpret_cast<const uint4*>(stage + (S::kKChunks + dt) * 1024 + lane * 16);
+}
+
+// Per-lane view of up to 64 block entries of a unit: lane i holds entry i.
 struct Window {
-  int id, valid;
+  int id;     // physical block id (clamped into the pool)
+  int valid;  // valid tokens (0: skip)
+  int a, e;   // rows [a, e)
   float ks, vs;
 };
 
-template <int KV>
-__device__ __forceinline__ Window load_window(const Run& run, int w0, int lane, const AttnParams& p, bool* bad) {
-  Window w{-1, 0, 1.f, 1.f};
-  const int i = w0 + lane;
-  bool b = false;
-  if (i < run.nblk) {
-    int id = run.ids[run.first + i];
-    int v = kTok;
-    if (run.tail) {
-      v = run.len - (run.first + i) * kTok;
-      v = v < kTok ? v : kTok;
-      if (id < 0 || id >= p.num_blocks) {
-        b = true;
-        id = -1;
-        v = 0;
-      }
-    }
-    w.id = id;
-    w.valid = v;
-    if constexpr (KV == kKvFp8) {
-      if (id >= 0) {
-        w.ks = p.k_scale[id];
-        w.vs = p.v_scale[id];
-      }
-    }
-  }
-  if (__builtin_amdgcn_ballot_w64(b) != 0) *bad = true;
-  return w;
+__device__ __forceinline__ int ent_r0(uint32_t inf) { return inf & 63; }
+__device__ __forceinline__ int ent_r1(uint32_t inf) { return ((inf >> 6) & 63) + 1; }
+__device__ __forceinline__ int ent_valid(uint32_t inf) { return ((inf >> 12) & 15) + 1; }
+
+// Loads of pair pp of a window (n entries) into f.
+template <int D, int KV>
+__device__ __forceinline__ void issue_pair(Frags<D, KV>& f, const Window& win, int n, int pp,
+                                           const unsigned char* kbase, const unsigned char* vbase, size_t blk_stride,
+                                           int ln, int lq, bool standin = false) {
+  const int i0 = 2 * pp, i1 = 2 * pp + 1;
+  const int id0 = rl(win.id, i0);
+  const int id1 = i1 < n ? rl(win.id, i1) : id0;
+  load_pair<D, KV>(f, kbase + id0 * blk_stride, kbase + id1 * blk_stride, vbase + id0 * blk_stride,
+                   vbase + id1 * blk_stride, ln, lq, standin);
 }
 
-// Workgroup barrier for the staged pipeline: LDS writes of this wave have
-// completed, then s_barrier. Unlike __syncthreads() it does not wait for
-// outstanding global loads (whose results are still travelling to their
-// registers), which is what keeps several pairs in flight across it.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// Runs every pair of a window (n entries) through the unit's row tiles
+// (rows outside a block's range are masked); pairs w, w + 4, ... belong to
+// wave w. The next pair's loads are issued before the current pair is
+// computed; the wave's first pair has been issued into fa by the caller.
+template <int D, int KV>
+__device__ __forceinline__ void run_window(const Window& win, int n, int nt, const unsigned char* kbase,
+                                           const unsigned char* vbase, size_t blk_stride, float sc,
+                                           const unsigned char* qlds, RowState<D> (&st)[kTiles],
+                                           Frags<D, KV>& fa, int wave, int ln, int lq) {
+  const int np = (n + 1) >> 1;
+  if (wave >= np) return;
+  auto info = [&](int pp) {
+    PairInfo pi;
+    const int i0 = 2 * pp, i1 = 2 * pp + 1;
+    const bool has1 = i1 < n;
+    pi.v0 = rl(win.valid, i0);
+    pi.v1 = has1 ? rl(win.valid, i1) : 0;
+    pi.a0 = rl(win.a, i0);
+    pi.e0 = rl(win.e, i0);
+    pi.a1 = has1 ? rl(win.a, i1) : 0;
+    pi.e1 = has1 ? rl(win.e, i1) : 0;
+    pi.ks0 = sc;
+    pi.ks1 = sc;
+    pi.vs0 = 1.f;
+    pi.vs1 = 1.f;
+    if constexpr (KV == kKvFp8) {
+      pi.ks0 = sc * rlf(win.ks, i0);
+      pi.vs0 = rlf(win.vs, i0);
+      pi.ks1 = has1 ? sc * rlf(win.ks, i1) : pi.ks0;
+      pi.vs1 = has1 ? rlf(win.vs, i1) : pi.vs0;
+    }
+    return pi;
+  };
+  auto tiles = [&](Ops<D, KV>& o, const PairInfo& pi) {
+    if (pi.v0 < kTok || pi.v1 < kTok) mask_v<D, KV>(o, lq, pi.v0, pi.v1);
+    // Row tiles the pair's valid blocks apply to.
+    int lo = kMaxRows, hi = 0;
+    if (pi.v0 > 0) {
+      lo = pi.a0;
+      hi = pi.e0;
+    }
+    if (pi.v1 > 0) {
+      lo = lo < pi.a1 ? lo : pi.a1;
+      hi = hi > pi.e1 ? hi : pi.e1;
+    }
+    const int t0 = lo >> 4, t1 = (hi - 1) >> 4;
+#pragma unroll
+    for (int r = 0; r < kTiles; ++r)
+      if (r < nt && r >= t0 && r <= t1) tile_step<D, KV>(o, q_from_lds<D, KV>(qlds, r, ln, lq), st[r], pi, r, ln, lq);
+  };
+  auto compute = [&](Frags<D, KV>& f, int pp) {
+    const PairInfo pi = info(pp);
+    if (pi.v0 <= 0 && pi.v1 <= 0) return;
+    if constexpr (KV == kKvFp8) {
+      Ops<D, KV> o;
+      fp8_to_ops<D>(f, o);
+      tiles(o, pi);
+    } else {
+      tiles(f, pi);
+    }
+  };
+  auto issue = [&](Frags<D, KV>& f, int pp, bool standin) {
+    issue_pair<D, KV>(f, win, n, pp, kbase, vbase, blk_stride, ln, lq, standin);
+  };
+  // The next pair's loads are always issued (constant wait counts); past the
+  // wave's last pair they are stand-ins that all read the first 16 bytes of
+  // the pair just loaded (a cache hit), so later waits on them are short.
+  Frags<D, KV> fb;
+  int pp = wave;
+  for (;;) {
+    int pn = pp + kWaves;
+    bool more = pn < np;
+    issue(fb, more ? pn : pp, !more);
+    compute(fa, pp);
+    if (!more) break;
+    pp = pn;
+    pn = pp + kWaves;
+    more = pn < np;
+    issue(fa, more ? pn : pp, !more);
+    compute(fb, pp);
+    if (!more) break;
+    pp = pn;
+  }
+}
 
-__device__ __forceinline__ int rl(int x, int i) { return __builtin_amdgcn_readlane(x, i); }
-__device__ __forceinline__ float rlf(float x, int i) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), i));
+// A unit's record as held by a wave: header fields (every lane holds the
+// same value; made uniform with readfirstlane where used, so that a record
+// fetched ahead of time is not waited for early) and, per lane, beam `lane`
+// (lane < 16) and entry `lane`.
+struct UnitRegs {
+  int kvh, nrows, nstatic, nent, prow0, next, mode;
+  int beam_l;
+  int ent_id;
+  uint32_t ent_inf;
+};
+
+__device__ __forceinline__ int rfl(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ __forceinline__ UnitRegs load_unit(const UnitRec* recs, int idx, int lane) {
+  const UnitRec* r = recs + idx;
+  UnitRegs u;
+  const int4 h0 = *reinterpret_cast<const int4*>(&r->kvh);
+  const int4 h1 = *reinterpret_cast<const int4*>(&r->prow0);
+  u.kvh = h0.x;
+  u.nrows = h0.y;
+  u.nstatic = h0.z;
+  u.nent = h0.w;
+  u.prow0 = h1.x;
+  u.next = h1.y;
+  u.mode = h1.z;
+  u.beam_l = r->beams[lane];
+  u.ent_id = r->ent_id[lane];
+  u.ent_inf = r->ent_info[lane];
+  return u;
+}
+
+// Live and build-time lengths of the beams whose entries depend on them
+// (the partial last block, the extension marker), loaded by those lanes.
+__device__ __forceinline__ void issue_live(const AttnParams& p, const UnitRegs& u, int lane, int* len, int* build) {
+  const bool live = lane < u.nent && (u.ent_inf & (kEntLive | kEntExt)) != 0;
+  const int slot = (u.ent_inf & kEntExt) ? u.ent_id : static_cast<int>(ent_r0(u.ent_inf)) / p.g;
+  const int lb = __shfl(u.beam_l, slot & 15);  // all lanes take part in the shuffle
+  *len = 0;
+  *build = 0;
+  if (live) {
+    *len = p.seq_lens[lb];
+    *build = p.build_len[lb];
+  }
+}
+
+// The unit's query rows, fetched into registers (thread t holds 16-byte
+// chunks t, t + 256, ... of the rows) while the previous unit finishes, then
+// stored to LDS in the swizzled layout. Rows past nrows repeat row 0 (their
+// scores are always masked).
+// (A vector value rather than an array, so that it stays in registers.)
+template <int D, int KV>
+struct QRegs {
+  static constexpr int kPer = QLds<D, KV>::bytes / (kThreads * 16);
+  typedef unsigned int V __attribute__((ext_vector_type(4 * kPer)));
+  V v;
+};
+
+template <int D, int KV>
+__device__ __forceinline__ void load_q(const AttnParams& p, const UnitRegs& u, QRegs<D, KV>& qr, int tid) {
+  using Q = QLds<D, KV>;
+#pragma unroll
+  for (int i = 0; i < QRegs<D, KV>::kPer; ++i) {
+    const int c = tid + kThreads * i;
+    int row = c / Q::ncol;
+    const int col = c % Q::ncol;
+    row = row < u.nrows ? row : 0;
+    const int b = __shfl(u.beam_l, row / p.g);
+    const int qh = u.kvh * p.g + row % p.g;
+    const uint4 t = *reinterpret_cast<const uint4*>(static_cast<const unsigned char*>(p.q) +
+                                                    (static_cast<int64_t>(b) * p.hq + qh) * Q::row_bytes + col * 16);
+    qr.v[4 * i] = t.x;
+    qr.v[4 * i + 1] = t.y;
+    qr.v[4 * i + 2] = t.z;
+    qr.v[4 * i + 3] = t.w;
+  }
 }
 
 template <int D, int KV>
-__global__ __launch_bounds__(kThreads, 2) void attn_units_kernel(AttnParams p) {
+__device__ __forceinline__ void store_q(const QRegs<D, KV>& qr, unsigned char* qbuf, int tid) {
+  using Q = QLds<D, KV>;
+#pragma unroll
+  for (int i = 0; i < QRegs<D, KV>::kPer; ++i) {
+    const int c = tid + kThreads * i;
+    *reinterpret_cast<uint4*>(qbuf + Q::offset(c / Q::ncol, c % Q::ncol)) =
+        uint4{qr.v[4 * i], qr.v[4 * i + 1], qr.v[4 * i + 2], qr.v[4 * i + 3]};
+  }
+}
+
+template <int D, int KV>
+__global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
   using G = Geo<D, KV>;
-  using F = PairFrags<D, KV>;
-  // Four distinct LDS stages (the last two are stubs when only two are used).
-  __shared__ __attribute__((aligned(16))) unsigned char lds_s0[G::stage_alloc];
-  __shared__ __attribute__((aligned(16))) unsigned char lds_s1[G::stage_alloc];
-  __shared__ __attribute__((aligned(16))) unsigned char lds_s2[G::stages > 2 ? G::stage_alloc : 16];
-  __shared__ __attribute__((aligned(16))) unsigned char lds_s3[G::stages > 3 ? G::stage_alloc : 16];
-  // Stage i (i is a compile-time constant wherever this is used).
-  auto stage_of = [&](int i) -> unsigned char* {
-    return i == 0 ? lds_s0 : (i == 1 ? lds_s1 : (i == 2 ? lds_s2 : lds_s3));
-  };
+  using Q = QLds<D, KV>;
+  // LDS: the current unit's query rows, and the end-of-unit combine area
+  // where each wave publishes the states of the row tiles other waves
+  // combine (3 x 4 (wave, tile) slots).
+  // Wide units (bf16) use the area after the query rows for their pair
+  // stages instead.
+  constexpr int kCombBytes = kWaves * (kTiles - 1) * G::comb_floats * 4;
+  constexpr int kStageBytes = KV == kKvBf16 ? 2 * Stage<D, KV>::bytes : 0;
+  constexpr int kAreaBytes = kCombBytes > kStageBytes ? kCombBytes : kStageBytes;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[Q::bytes + kAreaBytes];
+  unsigned char* qbuf = lds;
+  float* comb = reinterpret_cast<float*>(lds + Q::bytes);
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
   const int lane = tid & 63;
   const int ln = lane & 15;
   const int lq = lane >> 4;
+  const size_t blk_stride = static_cast<size_t>(p.hkv) * G::blk_bytes;
+  const bool paged = p.recs == nullptr;
+  const float sc_w = p.scale_log2;
+  const float sc = p.scale_log2;
+  auto comb_slot = [&](int w, int r) {  // (wave w, tile r != w)
+    return comb + (w * (kTiles - 1) + (r < w ? r : r - 1)) * G::comb_floats;
+  };
 
-  TTS_PROF_MARK(0);
-  // ---- the unit ----------------------------------------------------------
-  Unit u;
-  if (p.units) {
-    u = p.units[blockIdx.x];
-    if (u.nrows <= 0) return;  // padding unit
-  } else {  // paged path: unit = (beam, kv head, split), no sharing
-    const int j = blockIdx.x % p.paged_nsplit;
+  // ---- first unit -----------------------------------------------------------
+  int rec_idx;
+  UnitRegs u;
+  int paged_b = 0, paged_split = 0;
+  if (!paged) {
+    rec_idx = static_cast<int>(blockIdx.x);
+    u = load_unit(p.recs, rec_idx, lane);
+  } else {
+    // Paged path: unit = (beam, KV head, split) from the workgroup id, one
+    // beam's g rows against up to 64 of its blocks.
+    rec_idx = 0;
+    paged_split = blockIdx.x % p.paged_nsplit;
     const int bh = blockIdx.x / p.paged_nsplit;
+    paged_b = bh / p.hkv;
     u.kvh = bh % p.hkv;
-    u.kind = kTailSplit;
-    u.pos0 = bh / p.hkv;
-    u.nbeams = 1;
-    u.row0 = 0;
     u.nrows = p.g;
-    u.blk_off = j;
-    u.nblk = p.paged_nsplit;
-    u.slot = j;
+    u.nstatic = 0;
+    u.nent = 0;
+    u.prow0 = 0;
+    u.next = -1;
+    u.mode = kModeNarrow;
+    u.beam_l = paged_b;
+    u.ent_id = 0;
+    u.ent_inf = 0;
   }
-
-  Run run;
-  bool bad = false;
-  run.len = 0;
-  if (u.kind == kSegmentPiece) {
-    run.tail = false;
-    run.ids = p.seg_blocks;
-    run.first = u.blk_off;
-    run.nblk = u.nblk;
-  } else {
-    run.tail = true;
-    const int b = p.perm ? p.perm[u.pos0] : u.pos0;
-    const int L = p.seq_lens[b];
-    const int t0 = p.tail_lblock ? p.tail_lblock[b] : 0;
-    int nb_all = (L + kTok - 1) / kTok;
-    if (L < 0 || nb_all > p.max_blocks || (!p.perm && L > p.paged_max_len) || nb_all < t0) {
-      bad = true;
-      nb_all = t0;
+  if (rfl(u.nrows) <= 0) return;
+  QRegs<D, KV> qr;
+  load_q<D, KV>(p, u, qr, tid);
+  Frags<D, KV> fa;
+  bool fa_ready = false;  // the unit's first pair, lengths and next record are in flight
+  int ext_len = 0, ext_build = 0;  // live / extension lanes: live and build-time length
+  UnitRegs nu;
+  // Hand-over to unit n: a narrow unit's query rows, first pair and lengths
+  // go out before this unit's combine. Every path assigns the carried
+  // registers, so their previous contents are dead while a unit runs.
+  auto handover = [&](const UnitRegs& n) {
+    if (rfl(n.mode) == kModeNarrow) {
+      load_q<D, KV>(p, n, qr, tid);
+      const int nn = rfl(n.nstatic), nkvh = rfl(n.kvh);
+      Window nw;
+      nw.id = n.ent_id;
+      issue_pair<D, KV>(fa, nw, nn > 0 ? nn : 1, wave < ((nn + 1) >> 1) ? wave : 0,
+                        static_cast<const unsigned char*>(p.k_cache) + nkvh * G::blk_bytes,
+                        static_cast<const unsigned char*>(p.v_cache) + nkvh * G::blk_bytes, blk_stride, ln, lq,
+                        wave >= ((nn + 1) >> 1));
+      issue_live(p, n, lane, &ext_len, &ext_build);
+    } else {
+      qr = QRegs<D, KV>{};
+      fa = Frags<D, KV>{};
+      ext_len = 0;
+      ext_build = 0;
     }
-    const int tb = nb_all - t0;
-    // Splits cover whole pairs so only a sequence's last pair is ragged.
-    const int npairs = (tb + 1) >> 1;
-    const int per = 2 * ((npairs + u.nblk - 1) / u.nblk);
-    int a = t0 + u.blk_off * per;
-    int e = a + per;
-    if (e > nb_all) e = nb_all;
-    if (a > e) a = e;
-    run.ids = p.block_tables + static_cast<int64_t>(b) * p.max_blocks;
-    run.first = a;
-    run.nblk = e - a;
-    run.len = L;
-  }
+    fa_ready = true;
+  };
 
-  // ---- wave roles --------------------------------------------------------
-  const int nrt = (u.nrows + 15) >> 4;
-  const int wr = nrt >= 3 ? 4 : nrt;  // waves splitting rows
-  const int wt = kWaves / wr;         // waves splitting block pairs
-  const int rt = wave % wr;
-  const int tl = wave / wr;
-  const int rloc = rt * 16 + ln;
-  const bool row_ok = rloc < u.nrows;
-  const bool wave_active = rt * 16 < u.nrows;
-  int beam, qh;
-  {
-    const int r = u.row0 + (row_ok ? rloc : 0);
-    const int pos = u.pos0 + r / p.g;
-    beam = p.perm ? p.perm[pos] : pos;
-    qh = u.kvh * p.g + r % p.g;
-  }
+  for (;;) {
+    TTS_PROF_MARK(0, rec_idx);
+    const int kvh = rfl(u.kvh), nrows = rfl(u.nrows), nent = rfl(u.nent), prow0 = rfl(u.prow0),
+              unext = rfl(u.next);
+    const int nt = (nrows + 15) >> 4;
+    const unsigned char* kbase = static_cast<const unsigned char*>(p.k_cache) + kvh * G::blk_bytes;
+    const unsigned char* vbase = static_cast<const unsigned char*>(p.v_cache) + kvh * G::blk_bytes;
 
-  // ---- query fragments (B operand of S^T = K Q^T) ------------------------
-  typename F::KF qf[F::kk];
-  if constexpr (KV == kKvF32) {
-    const float* qrow = static_cast<const float*>(p.q) + (static_cast<int64_t>(beam) * p.hq + qh) * D;
+    if constexpr (KV == kKvBf16) {
+      if (rfl(u.mode) == kModeWide) {
+        // ---- wide unit: wave w owns row tiles w, w + 4, ...; every block
+        // pair is copied to an LDS stage once and read by all four waves ---
+        using SG = Stage<D, KV>;
+        const int nst = rfl(u.nstatic);
+        nu.nrows = 0;
+        if (unext >= 0) nu = load_unit(p.recs, unext, lane);
+        QFrag<D, KV> qw[kWideTiles];
 #pragma unroll
-    for (int j = 0; j < F::kk; ++j)
-      qf[j] = row_ok ? *reinterpret_cast<const f32x4*>(qrow + 16 * j + 4 * lq) : f32x4{0.f, 0.f, 0.f, 0.f};
-  } else {
-    const uint16_t* qrow = static_cast<const uint16_t*>(p.q) + (static_cast<int64_t>(beam) * p.hq + qh) * D;
+        for (int i = 0; i < kWideTiles; ++i) {
+          const int row = 16 * (wave + kWaves * i) + ln;
+          const bool ok = row < nrows;
+          const int b = __shfl(u.beam_l, ok ? row / p.g : 0);
+          const int qh = kvh * p.g + (ok ? row % p.g : 0);
+          const uint16_t* qrow = static_cast<const uint16_t*>(p.q) + (static_cast<int64_t>(b) * p.hq + qh) * D;
 #pragma unroll
-    for (int j = 0; j < F::kk; ++j)
-      qf[j] = row_ok ? *reinterpret_cast<const uint4*>(qrow + 32 * j + 8 * lq) : uint4{0u, 0u, 0u, 0u};
-  }
-
-  RowState<D> st;
-#pragma unroll
-  for (int i = 0; i < D / 16; ++i) st.o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  st.m = kNegInf;
-  st.l = 0.f;
-
-  const size_t kv_blk_stride = static_cast<size_t>(p.hkv) * G::blk_bytes;
-  const unsigned char* kbase_g = static_cast<const unsigned char*>(p.k_cache) + u.kvh * G::blk_bytes;
-  const unsigned char* vbase_g = static_cast<const unsigned char*>(p.v_cache) + u.kvh * G::blk_bytes;
-  const float sc_log2 = p.scale_log2;
-
-  if (nrt == 1) {
-    // ---- direct path: each wave streams its own block pairs -------------
-    for (int w0 = 0; w0 < run.nblk; w0 += 64) {
-      const Window win = load_window<KV>(run, w0, lane, p, &bad);
-      const int nw = (run.nblk - w0) < 64 ? (run.nblk - w0) : 64;
-      const int npairs = (nw + 1) >> 1;
-      for (int pp = tl; pp < npairs; pp += wt) {
-        const int i0 = 2 * pp, i1 = 2 * pp + 1;
-        const int v0 = rl(win.valid, i0);
-        const int v1 = i1 < nw ? rl(win.valid, i1) : 0;
-        if (v0 <= 0 && v1 <= 0) continue;
-        const int id0 = rl(win.id, i0);
-        const int id1 = i1 < nw ? rl(win.id, i1) : -1;
-        // A missing or bad block re-reads a valid one and is fully masked.
-        const int r0 = v0 > 0 ? id0 : id1;
-        const int r1 = v1 > 0 ? id1 : r0;
-        F f;
-        load_k_global<D, KV>(f, kbase_g + r0 * kv_blk_stride, kbase_g + r1 * kv_blk_stride, ln, lq);
-        load_v<D, KV>(f, vbase_g + r0 * kv_blk_stride, vbase_g + r1 * kv_blk_stride, ln, lq);
-        float ks0 = 1.f, ks1 = 1.f, vs0 = 1.f, vs1 = 1.f;
-        if constexpr (KV == kKvFp8) {
-          ks0 = rlf(win.ks, v0 > 0 ? i0 : i1);
-          vs0 = rlf(win.vs, v0 > 0 ? i0 : i1);
-          ks1 = v1 > 0 ? rlf(win.ks, i1) : ks0;
-          vs1 = v1 > 0 ? rlf(win.vs, i1) : vs0;
+          for (int j = 0; j < Ops<D, KV>::kk; ++j)
+            qw[i].q[j] = ok ? *reinterpret_cast<const uint4*>(qrow + 32 * j + 8 * lq) : uint4{0u, 0u, 0u, 0u};
         }
-        const bool masked = v0 < kTok || v1 < kTok;
-        if (masked) mask_v<D, KV>(f, lq, v0, v1);
-        pair_step<D, KV>(f, qf, st, lq, sc_log2 * ks0, sc_log2 * ks1, vs0, vs1, v0, v1, masked);
-      }
-    }
-  } else {
-    // ---- staged path: pairs land in LDS, every wave reads them -----------
-    // Each stage holds K0, V0, K1, V1 of one pair; wave w copies tensor w
-    // straight from global memory into LDS (no registers). The stages are
-    // distinct LDS objects indexed at compile time so that the compiler does
-    // not make reads of one stage wait for copies into another; kStages - 2
-    // pairs stay in flight across each barrier.
-    constexpr int kStages = G::stages;
-    constexpr int kDma = G::dma_per_wave;
-    const bool is_v = wave & 1;
-    const int blk_sel = wave >> 1;
-    for (int w0 = 0; w0 < run.nblk; w0 += 64) {
-      const Window win = load_window<KV>(run, w0, lane, p, &bad);
-      __builtin_amdgcn_s_waitcnt(0x0F70);  // window and query loads done
-      const int nw = (run.nblk - w0) < 64 ? (run.nblk - w0) : 64;
-      const int npairs = (nw + 1) >> 1;
-      // Any valid block of the window stands in for invalid ones (loaded, never used).
-      const uint64_t any_valid = __builtin_amdgcn_ballot_w64(lane < nw && win.valid > 0);
-      if (any_valid == 0) continue;  // uniform: nothing to read in this window
-      const int fill_id = rl(win.id, static_cast<int>(__builtin_ctzll(any_valid)));
-      auto pair_ids = [&](int pp, int* r0, int* r1, int* v0, int* v1) {
-        const int i0 = 2 * pp, i1 = 2 * pp + 1;
-        *v0 = rl(win.valid, i0);
-        *v1 = i1 < nw ? rl(win.valid, i1) : 0;
-        const int id0 = rl(win.id, i0);
-        const int id1 = i1 < nw ? rl(win.id, i1) : -1;
-        *r0 = *v0 > 0 ? id0 : (*v1 > 0 ? id1 : fill_id);
-        *r1 = *v1 > 0 ? id1 : *r0;
-      };
-      // Copy pair pp (clamped to the window) into stage `dst`: always exactly
-      // kDma loads per wave, so the wait counts below are constants.
-      auto issue = [&](int pp, unsigned char* dst) {
-        pp = pp < npairs ? pp : npairs - 1;
-        int r0, r1, v0, v1;
-        pair_ids(pp, &r0, &r1, &v0, &v1);
-        const int rid = blk_sel ? r1 : r0;
-        const unsigned char* src = (is_v ? vbase_g : kbase_g) + static_cast<size_t>(rid) * kv_blk_stride;
-        unsigned char* d = dst + wave * G::blk_bytes;
+        unsigned char* stages = lds + Q::bytes;
+        const int np = (nst + 1) >> 1;
+        auto pair_ids = [&](int pp, int* id0, int* id1) {
+          pp = pp < np ? pp : np - 1;  // past the end: a repeat of the last pair (a cache hit, never used)
+          *id0 = rl(u.ent_id, 2 * pp);
+          *id1 = 2 * pp + 1 < nst ? rl(u.ent_id, 2 * pp + 1) : *id0;
+        };
+        RowState<D> st[kWideTiles];
+        float m_exact[kWideTiles];
 #pragma unroll
-        for (int j = 0; j < kDma; ++j) {
-          const int pos = j * 64 + lane;  // 16-byte slot of this lane in the tensor
-          int off;
-          if (!is_v) {
-            const int r = pos / G::c16;
-            off = r * G::row_bytes + (((pos % G::c16) ^ k_swz<G::c16>(blk_sel, r)) << 4);
-          } else if constexpr (KV == kKvBf16) {
-            const int dd = pos >> 1;
-            off = dd * G::vrow_bytes + 16 * ((pos & 1) ^ v_half_swz(dd));
-          } else {
-            off = pos * 16;
+        for (int i = 0; i < kWideTiles; ++i) m_exact[i] = 0.f;
+        for (int attempt = 0;; ++attempt) {
+#pragma unroll
+          for (int i = 0; i < kWideTiles; ++i) {
+#pragma unroll
+            for (int d = 0; d < D / 16; ++d) st[i].o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+            st[i].m = m_exact[i];
+            st[i].l = 0.f;
+            st[i].seen = kNegInf;
           }
-          __builtin_amdgcn_global_load_lds(src + off, (__attribute__((address_space(3))) void*)(d + j * 1024),
-                                           16, 0, 0);
-        }
-      };
-      auto consume = [&](int pp, const unsigned char* stage) {
-        int r0, r1, v0, v1;
-        pair_ids(pp, &r0, &r1, &v0, &v1);
-        if (!wave_active || (pp % wt) != tl || (v0 <= 0 && v1 <= 0)) return;
-        F f;
-        load_pair_lds<D, KV>(f, stage, stage + 2 * G::blk_bytes, stage + G::blk_bytes, stage + 3 * G::blk_bytes, ln,
-                             lq);
-        float ks0 = 1.f, ks1 = 1.f, vs0 = 1.f, vs1 = 1.f;
-        if constexpr (KV == kKvFp8) {
-          const int i0 = 2 * pp, i1 = 2 * pp + 1;
-          ks0 = rlf(win.ks, v0 > 0 ? i0 : i1);
-          vs0 = rlf(win.vs, v0 > 0 ? i0 : i1);
-          ks1 = v1 > 0 ? rlf(win.ks, i1) : ks0;
-          vs1 = v1 > 0 ? rlf(win.vs, i1) : vs0;
-        }
-        const bool masked = v0 < kTok || v1 < kTok;
-        if (masked) mask_v<D, KV>(f, lq, v0, v1);
-        pair_step<D, KV>(f, qf, st, lq, sc_log2 * ks0, sc_log2 * ks1, vs0, vs1, v0, v1, masked);
-      };
+          Quarter<D, KV> qa, qb;
+          int id0, id1;
+          pair_ids(0, &id0, &id1);
+          load_quarter<D, KV>(qa, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
+          __syncthreads();  // every wave is done with the stage area (previous unit or attempt)
+          auto step = [&](Quarter<D, KV>& cur, Quarter<D, KV>& nxt, int pp) {
+            pair_ids(pp + 1, &id0, &id1);
+            load_quarter<D, KV>(nxt, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
+            unsigned char* stage = stages + (pp & 1) * SG::bytes;
+            store_quarter<D, KV>(cur, stage, wave, lane);
+            __syncthreads();  // the whole pair is in the stage
+            Ops<D, KV> o;
+            read_stage<D, KV>(o, stage, lane);
+            PairInfo pi;
+            pi.v0 = kTok;
+            pi.v1 = 2 * pp + 1 < nst ? kTok : 0;
+            pi.a0 = pi.a1 = 0;
+            pi.e0 = pi.e1 = nrows;
+            pi.ks0 = pi.ks1 = sc_w;
+            pi.vs0 = pi.vs1 = 1.f;
+            if (pi.v1 == 0) mask_v<D, KV>(o, lq, pi.v0, pi.v1);
 #pragma unroll
-      for (int j = 0; j < kStages - 1; ++j) issue(j, stage_of(j));
-      for (int p0 = 0; p0 < npairs; p0 += kStages) {
+            for (int i = 0; i < kWideTiles; ++i)
+              if (wave + kWaves * i < nt) tile_step<D, KV>(o, qw[i], st[i], pi, wave + kWaves * i, ln, lq);
+          };
+          for (int pp = 0; pp < np; pp += 2) {
+            step(qa, qb, pp);
+            if (pp + 1 >= np) break;
+            step(qb, qa, pp + 1);
+          }
+          if (attempt == 0) TTS_PROF_MARK(1, rec_idx);
+          if (attempt > 0) break;
+          bool redo = false;
 #pragma unroll
-        for (int s = 0; s < kStages; ++s) {
-          const int pp = p0 + s;
-          if (pp < npairs) {
-            // Pairs pp + 1 .. pp + kStages - 2 may still be in flight.
-            __builtin_amdgcn_s_waitcnt(0x0F70 | (((kStages - 2) * kDma) & 15) | ((((kStages - 2) * kDma) >> 4) << 14));
-            lds_barrier();
-            issue(pp + kStages - 1, stage_of((s + kStages - 1) % kStages));
-            consume(pp, stage_of(s));
+          for (int i = 0; i < kWideTiles; ++i) {
+            const float mx = xlane_max16(st[i].seen);
+            redo |= mx > kRefWindow || (mx < -kRefWindow && mx != kNegInf);
+            m_exact[i] = mx == kNegInf ? 0.f : mx;
+          }
+          if (__builtin_amdgcn_ballot_w64(redo) == 0) break;
+        }
+        // Each wave writes the partial states of its own rows.
+#pragma unroll
+        for (int i = 0; i < kWideTiles; ++i) {
+          const int row = 16 * (wave + kWaves * i) + ln;
+          const float l = xlane_sum16(st[i].l);
+          if (row < nrows) {
+            const int64_t prow = static_cast<int64_t>(kvh) * p.rows_per_head + prow0 + row;
+            float* po = p.part_o + prow * D;
+#pragma unroll
+            for (int d = 0; d < D / 16; ++d) *reinterpret_cast<f32x4*>(po + 16 * d + 4 * lq) = st[i].o[d];
+            if (lq == 0) *reinterpret_cast<f32x2*>(p.part_ml + prow * 2) = f32x2{st[i].m, l};
           }
         }
+        TTS_PROF_MARK(2, rec_idx);
+        const int nu_rows_w = rfl(nu.nrows);
+        if (nu_rows_w <= 0) break;
+        handover(nu);
+        rec_idx = unext;
+        u = nu;
+        continue;
       }
-      __builtin_amdgcn_s_waitcnt(0x0F70);  // the clamped trailing copies
-      __syncthreads();                      // every wave is done with the stages
     }
-  }
 
-  TTS_PROF_MARK(1);
-  // A bad block id may have been seen by one wave only.
-  bad = __syncthreads_or(bad ? 1 : 0) != 0;
+    // ---- the unit's block window ------------------------------------------
+    Window win;
+    uint64_t bad_rows = 0;  // rows that met a bad block id or an over-long beam: NaN
+    int nstatic = rfl(u.nstatic);
+    if (!paged) {
+      win.id = u.ent_id;
+      win.a = ent_r0(u.ent_inf);
+      win.e = ent_r1(u.ent_inf);
+      win.valid = lane < nstatic ? ent_valid(u.ent_inf) : 0;
+      if (!fa_ready) issue_live(p, u, lane, &ext_len, &ext_build);
+    } else {
+      const int L = p.seq_lens[paged_b];
+      // Split j covers blocks [j * per, (j + 1) * per) of the beam (per <= 64).
+      const int per = (p.paged_max_len + kTok * p.paged_nsplit - 1) / (kTok * p.paged_nsplit);
+      const int j = paged_split * per + lane;
+      int nb = (L + kTok - 1) / kTok;
+      bool bad = false;
+      if (L < 0 || L > p.paged_max_len || nb > p.max_blocks) {
+        bad = true;
+        nb = 0;
+      }
+      nstatic = nb - paged_split * per;
+      nstatic = nstatic < 0 ? 0 : (nstatic < per ? nstatic : per);
+      int id = 0, v = 0;
+      if (lane < nstatic) {
+        id = p.block_tables[static_cast<int64_t>(paged_b) * p.max_blocks + j];
+        v = L - j * kTok;
+        v = v < kTok ? v : kTok;
+        if (id < 0 || id >= p.num_blocks) {
+          bad = true;
+          id = 0;
+          v = 0;
+        }
+      }
+      win.id = id;
+      win.valid = v;
+      win.a = 0;
+      win.e = nrows;
+      if (__builtin_amdgcn_ballot_w64(bad) != 0) bad_rows = ~0ull;
+    }
+    win.ks = 1.f;
+    win.vs = 1.f;
+    if constexpr (KV == kKvFp8) {
+      if (win.valid > 0) {
+        win.ks = p.k_scale[win.id];
+        win.vs = p.v_scale[win.id];
+      }
+    }
+    if (!fa_ready && wave < ((nstatic + 1) >> 1))
+      issue_pair<D, KV>(fa, win, nstatic, wave, kbase, vbase, blk_stride, ln, lq);
+    // The next unit's record: it has this unit's pair loop to arrive.
+    nu.nrows = 0;
+    if (unext >= 0) nu = load_unit(p.recs, unext, lane);
 
-  // ---- combine the waves that split block pairs --------------------------
-  float l_tot = xlane_sum16(st.l);
-  float m_fin = st.m;
-  if (wt > 1) {
-    // Waves 1..3 of a row tile publish their state in stages 0..2 (wt >= 2
-    // means at most two row tiles: slot = (tl - 1) * wr + rt < 3).
-    static_assert(G::stages > 2 || G::stage_alloc >= 2 * G::combine_bytes, "third combine slot");
-    auto region = [&](int t) {
-      const int slot = (t - 1) * wr + rt;
-      unsigned char* c = slot == 0 ? lds_s0 : (slot == 1 ? lds_s1 : (G::stages > 2 ? lds_s2 : lds_s0 + G::combine_bytes));
-      return reinterpret_cast<float*>(c);
-    };
-    float* my = tl > 0 ? region(tl) : nullptr;
-    // Rows are padded by 4 floats so the 16 lanes of a column hit distinct banks.
-    constexpr int kRow = D + 4;
-    if (tl > 0 && wave_active) {
+    store_q<D, KV>(qr, qbuf, tid);
+    __syncthreads();  // query rows in LDS
+
+    // ---- the unit's blocks with m_ref = 0; again with every row's exact
+    // maximum in the rare case that a row's maximum left the safe window ----
+    RowState<D> st[kTiles];
+    float m_exact[kTiles];
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) *reinterpret_cast<f32x4*>(my + ln * kRow + 16 * dt + 4 * lq) = st.o[dt];
-      if (lq == 0) {
-        my[kTok * kRow + ln] = st.m;
-        my[kTok * kRow + kTok + ln] = l_tot;
+    for (int r = 0; r < kTiles; ++r) m_exact[r] = 0.f;
+    if (!paged && lane < nstatic && (u.ent_inf & kEntLive)) {
+      // The beam's partial last block: it fills up as tokens are appended.
+      const int v = win.valid + (ext_len - ext_build);
+      win.valid = v < 0 ? 0 : (v > kTok ? kTok : v);
+    }
+    for (int attempt = 0;; ++attempt) {
+#pragma unroll
+      for (int r = 0; r < kTiles; ++r) {
+#pragma unroll
+        for (int i = 0; i < D / 16; ++i) st[r].o[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        st[r].m = m_exact[r];
+        st[r].l = 0.f;
+        st[r].seen = kNegInf;
+      }
+      if (attempt > 0 && wave < ((nstatic + 1) >> 1))
+        issue_pair<D, KV>(fa, win, nstatic, wave, kbase, vbase, blk_stride, ln, lq);
+      // Windows of blocks: the unit's own entries first, then (usually
+      // none) blocks its beams gained after the metadata was built, read
+      // from the live block table 64 at a time. One call site keeps the
+      // register allocation of the pair loop in one piece.
+      Window cw = win;
+      int cn = nstatic;
+      uint64_t ext_left = paged ? 0ull
+                                : __builtin_amdgcn_ballot_w64(lane >= nstatic && lane < nent &&
+                                                              (u.ent_inf & kEntExt) != 0);
+      int xb = 0, xnext = 0, xend = 0, xlen = 0, xa = 0, xe = 0;
+      for (;;) {
+        run_window<D, KV>(cw, cn, nt, kbase, vbase, blk_stride, sc, qbuf, st, fa, wave, ln, lq);
+        if (attempt == 0) TTS_PROF_MARK(1, rec_idx);
+        // Next extension window, if any.
+        while (xnext >= xend && ext_left != 0) {
+          const int e = static_cast<int>(__builtin_ctzll(ext_left));
+          ext_left &= ext_left - 1;
+          xlen = rl(ext_len, e);
+          const int B = rl(ext_build, e);
+          xb = __shfl(u.beam_l, rl(u.ent_id, e) & 15);
+          xa = rl(win.a, e);
+          xe = rl(win.e, e);
+          xnext = (B + kTok - 1) / kTok;
+          xend = (xlen + kTok - 1) / kTok;
+          if (xlen < B) {
+            xend = xnext;  // shorter than at build time: the merge reports NaN
+          } else if (xend > p.max_blocks) {
+            xend = xnext;  // longer than its table row: NaN rows
+            bad_rows |= (xe >= 64 ? ~0ull : ((1ull << xe) - 1)) & ~((1ull << xa) - 1);
+          }
+        }
+        if (xnext >= xend) break;
+        cn = (xend - xnext) < kMaxEntries ? (xend - xnext) : kMaxEntries;
+        int id = 0, v = 0;
+        bool xbad = false;
+        if (lane < cn) {
+          const int j = xnext + lane;
+          id = p.block_tables[static_cast<int64_t>(xb) * p.max_blocks + j];
+          v = xlen - j * kTok;
+          v = v < kTok ? v : kTok;
+          if (id < 0 || id >= p.num_blocks) {
+            xbad = true;
+            id = 0;
+            v = 0;
+          }
+        }
+        if (__builtin_amdgcn_ballot_w64(xbad) != 0)
+          bad_rows |= (xe >= 64 ? ~0ull : ((1ull << xe) - 1)) & ~((1ull << xa) - 1);
+        cw.id = id;
+        cw.valid = v;
+        cw.a = xa;
+        cw.e = xe;
+        cw.ks = 1.f;
+        cw.vs = 1.f;
+        if constexpr (KV == kKvFp8) {
+          if (v > 0) {
+            cw.ks = p.k_scale[id];
+            cw.vs = p.v_scale[id];
+          }
+        }
+        xnext += cn;
+        if (wave < ((cn + 1) >> 1)) issue_pair<D, KV>(fa, cw, cn, wave, kbase, vbase, blk_stride, ln, lq);
+      }
+      if (attempt > 0) break;
+      bool redo = false;
+#pragma unroll
+      for (int r = 0; r < kTiles; ++r) {
+        const float mx = xlane_max16(st[r].seen);
+        redo |= mx > kRefWindow || (mx < -kRefWindow && mx != kNegInf);
+        m_exact[r] = mx == kNegInf ? 0.f : mx;
+      }
+      if (__builtin_amdgcn_ballot_w64(redo) == 0) break;
+    }
+
+    // ---- hand over: the next unit's query copies and first pair go out
+    // before this unit's combine ---------------------------------------------
+    __syncthreads();  // every wave is done with qbuf
+    TTS_PROF_MARK(4, rec_idx);
+    const int nu_rows = rfl(nu.nrows);
+    if (nu_rows > 0) handover(nu);
+
+    TTS_PROF_MARK(5, rec_idx);
+    // ---- combine the four waves' states, tile r by wave r ------------------
+#pragma unroll
+    for (int r = 0; r < kTiles; ++r) {
+      if (r < nt && r != wave) {
+        float* c = comb_slot(wave, r);
+#pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt)
+          *reinterpret_cast<f32x4*>(c + ln * G::comb_row + 16 * dt + 4 * lq) = st[r].o[dt];
+        const float lt = xlane_sum16(st[r].l);
+        if (lq == 0) {
+          c[kTok * G::comb_row + ln] = st[r].m;
+          c[kTok * G::comb_row + kTok + ln] = lt;
+        }
       }
     }
     __syncthreads();
-    if (tl == 0 && wave_active) {
-      float mt[kWaves];
-      float mx = st.m;
-      mt[0] = st.m;
-      for (int t = 1; t < wt; ++t) {
-        mt[t] = region(t)[kTok * kRow + ln];
-        mx = fmaxf(mx, mt[t]);
-      }
-      const float mu = (mx == kNegInf) ? 0.f : mx;
-      const float f0 = (mt[0] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(mt[0] - mu);
-      l_tot *= f0;
+    TTS_PROF_MARK(6, rec_idx);
+    // Wave r combines tile r: its own state straight from registers (one
+    // code path per tile index, so nothing is copied), the other waves'
+    // from LDS, in wave order.
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) st.o[dt] *= f0;
-      for (int t = 1; t < wt; ++t) {
-        const float* ot = region(t);
-        const float fct = (mt[t] == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(mt[t] - mu);
-        l_tot += ot[kTok * kRow + kTok + ln] * fct;
+    for (int r = 0; r < kTiles; ++r) {
+      if (r != wave || r >= nt) continue;
+      const int row = 16 * r + ln;
+      const float own_l = xlane_sum16(st[r].l);
+      float mw[kWaves], mx = kNegInf;
 #pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt)
-          st.o[dt] += *reinterpret_cast<const f32x4*>(ot + ln * kRow + 16 * dt + 4 * lq) * fct;
+      for (int w = 0; w < kWaves; ++w) {
+        mw[w] = (w == r) ? st[r].m : comb_slot(w, r)[kTok * G::comb_row + ln];
+        mx = fmaxf(mx, mw[w]);
       }
-      m_fin = mx;
+      float l = 0.f;
+      f32x4 o[D / 16];
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const float f = __builtin_amdgcn_exp2f(mw[w] - mx);
+        if (w == r) {
+          l += own_l * f;
+#pragma unroll
+          for (int dt = 0; dt < D / 16; ++dt) o[dt] += st[r].o[dt] * f;
+        } else {
+          const float* c = comb_slot(w, r);
+          l += c[kTok * G::comb_row + kTok + ln] * f;
+#pragma unroll
+          for (int dt = 0; dt < D / 16; ++dt)
+            o[dt] += *reinterpret_cast<const f32x4*>(c + ln * G::comb_row + 16 * dt + 4 * lq) * f;
+        }
+      }
+      float m_fin = mx;
+      if ((bad_rows >> row) & 1ull) m_fin = __builtin_nanf("");
+      if (row < nrows) {
+        if (paged && p.paged_nsplit == 1) {
+          // Whole sequence in this unit: the normalised result.
+          float* orow = p.out + (static_cast<int64_t>(paged_b) * p.hq + kvh * p.g + row) * D;
+          const float inv = (l > 0.f) ? 1.f / l : 0.f;
+          const bool nan = m_fin != m_fin;
+#pragma unroll
+          for (int dt = 0; dt < D / 16; ++dt) {
+            f32x4 v = o[dt] * inv;
+            if (nan) v = f32x4{m_fin, m_fin, m_fin, m_fin};
+            *reinterpret_cast<f32x4*>(orow + 16 * dt + 4 * lq) = v;
+          }
+        } else {
+          int64_t prow;
+          if (paged)
+            prow = (static_cast<int64_t>(paged_b) * p.paged_nsplit + paged_split) * p.hq + kvh * p.g + row;
+          else
+            prow = static_cast<int64_t>(kvh) * p.rows_per_head + prow0 + row;
+          float* po = p.part_o + prow * D;
+#pragma unroll
+          for (int dt = 0; dt < D / 16; ++dt) *reinterpret_cast<f32x4*>(po + 16 * dt + 4 * lq) = o[dt];
+          if (lq == 0) *reinterpret_cast<f32x2*>(p.part_ml + prow * 2) = f32x2{m_fin, l};
+        }
+      }
     }
-  }
-  if (bad) m_fin = __builtin_nanf("");
-
-  // ---- write ---------------------------------------------------------------
-  const bool writer = tl == 0 && row_ok;
-  if (!p.units && p.paged_nsplit == 1) {
-    // Whole sequence in this unit: write the normalised result.
-    if (writer) {
-      float* orow = p.out + (static_cast<int64_t>(beam) * p.hq + qh) * D;
-      const float inv = (l_tot > 0.f) ? 1.f / l_tot : 0.f;
-      const bool nan = m_fin != m_fin;
-#pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
-        f32x4 v = st.o[dt] * inv;
-        if (nan) v = f32x4{m_fin, m_fin, m_fin, m_fin};
-        *reinterpret_cast<f32x4*>(orow + 16 * dt + 4 * lq) = v;
-      }
-    }
-    return;
-  }
-  if (writer) {
-    int64_t prow;
-    if (p.units)
-      prow = static_cast<int64_t>(p.slot_base[beam] + u.slot) * p.hq + qh;
-    else
-      prow = (static_cast<int64_t>(beam) * p.paged_nsplit + u.slot) * p.hq + qh;
-    float* po = p.part_o + prow * D;
-#pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) *reinterpret_cast<f32x4*>(po + 16 * dt + 4 * lq) = st.o[dt];
-    if (lq == 0) *reinterpret_cast<f32x2*>(p.part_ml + prow * 2) = f32x2{m_fin, l_tot};
-  }
 #ifdef TTS_PROFILE_UNITS
-  if (threadIdx.x == 0 && blockIdx.x < kProfSlots)
-    g_prof[blockIdx.x][3] = (static_cast<uint64_t>(__builtin_amdgcn_s_getreg((3 << 11) | 20)) << 32) |
-                            static_cast<uint32_t>(__builtin_amdgcn_s_getreg((31 << 11) | 4));
+    TTS_PROF_MARK(2, rec_idx);
+    if (threadIdx.x == 0 && rec_idx < kProfSlots)
+      g_prof[rec_idx][3] = (static_cast<uint64_t>(__builtin_amdgcn_s_getreg((3 << 11) | 20)) << 32) |
+                           static_cast<uint32_t>(__builtin_amdgcn_s_getreg((31 << 11) | 4));
 #endif
-  TTS_PROF_MARK(2);
+    if (nu_rows <= 0) break;
+    rec_idx = unext;
+    u = nu;
+    fa_ready = true;
+  }
 }
 
 // Exact merge of the partial softmax states of each (beam, query head), in
-// slot order (segments root to leaf, then tail splits):
+// the order of the beam's slot list:
 //   m = max_k m_k,  l = sum_k l_k 2^(m_k - m),  out = sum_k o_k 2^(m_k - m) / l.
-// D/4 threads share a row (4 output dims each) and issue the loads of up to
-// kBatch slots at once, so a row costs one round trip to memory per batch.
+// One wave per row (2 output dims per lane). A row's slot count and first
+// kMergeBatch slots sit in one row of the slot table and are loaded together
+// with the beam's lengths; then the states of kMergeBatch slots at a time,
+// so a row costs two round trips to memory (more only past kMergeBatch
+// slots).
 template <int D>
 __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
-  constexpr int kTpr = D / 4;
+  constexpr int kTpr = D / 2;
   constexpr int kRows = kThreads / kTpr;
-  constexpr int kBatch = 16;
+  constexpr int kBatch = kMergeBatch;
   const int r = blockIdx.x * kRows + threadIdx.x / kTpr;
-  const int d0 = (threadIdx.x % kTpr) * 4;
+  const int d0 = (threadIdx.x % kTpr) * 2;
   if (r >= p.num_seqs * p.hq) return;
   const int b = r / p.hq;
   const int h = r % p.hq;
-  int64_t base;
+  const int* tab = p.slot_tab ? p.slot_tab + static_cast<int64_t>(b) * p.slot_stride : nullptr;
   int n;
-  if (p.slot_base) {
-    base = p.slot_base[b];
-    n = p.slot_base[b + 1] - p.slot_base[b];
+  int ent[kBatch];
+  int64_t head_base;
+  if (tab) {
+    n = tab[0];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) ent[k] = tab[1 + k];
+    head_base = static_cast<int64_t>(h / p.g) * p.rows_per_head + h % p.g;
   } else {
-    base = static_cast<int64_t>(b) * p.paged_nsplit;
     n = p.paged_nsplit;
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) ent[k] = 0;
+    head_base = 0;
   }
   const int L = p.seq_lens[b];
-  bool nan = p.tail_lblock && L < p.tail_lblock[b] * kTok;
+  bool nan = p.build_len && L < p.build_len[b];
   float mx = kNegInf, l = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  f32x2 acc = {0.f, 0.f};
   for (int k0 = 0; k0 < n; k0 += kBatch) {
-    f32x2 ml[kBatch];
-    f32x4 o[kBatch];
+    if (k0 > 0 && tab) {
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) ent[k] = k0 + k < n ? tab[1 + k0 + k] : 0;
+    }
+    f32x2 ml[kBatch], o[kBatch];
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
       const int kk = k0 + k < n ? k0 + k : n - 1;
-      const int64_t row = (base + kk) * p.hq + h;
+      int64_t row;
+      if (tab)
+        row = head_base + (k0 + k < n ? ent[k] : ent[0]);
+      else
+        row = (static_cast<int64_t>(b) * p.paged_nsplit + kk) * p.hq + h;
       ml[k] = *reinterpret_cast<const f32x2*>(p.part_ml + row * 2);
-      o[k] = *reinterpret_cast<const f32x4*>(p.part_o + row * D + d0);
+      o[k] = *reinterpret_cast<const f32x2*>(p.part_o + row * D + d0);
     }
 #pragma unroll
     for (int k = 0; k < kBatch; ++k)
@@ -863,24 +1153,24 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
     mx = mn;
   }
   const float inv = (l > 0.f && L > 0) ? 1.f / l : 0.f;
-  f32x4 w = acc * inv;
+  f32x2 w = acc * inv;
   if (nan) {
     const float q = __builtin_nanf("");
-    w = f32x4{q, q, q, q};
+    w = f32x2{q, q};
   }
-  *reinterpret_cast<f32x4*>(p.out + static_cast<int64_t>(r) * D + d0) = w;
+  *reinterpret_cast<f32x2*>(p.out + static_cast<int64_t>(r) * D + d0) = w;
 }
 
 template <int D, int KV>
-static hipError_t launch_attn_t(const AttnParams& p, int num_units, hipStream_t stream) {
-  hipLaunchKernelGGL((attn_units_kernel<D, KV>), dim3(num_units), dim3(kThreads), 0, stream, p);
+static hipError_t launch_attn_t(const AttnParams& p, int grid, hipStream_t stream) {
+  hipLaunchKernelGGL((attn_kernel<D, KV>), dim3(grid), dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 
 hipError_t launch_merge(const MergeParams& p, int head_dim, hipStream_t stream) {
   const int rows = p.num_seqs * p.hq;
   if (rows <= 0) return hipSuccess;
-  const int per = kThreads / (head_dim / 4);
+  const int per = kThreads / (head_dim / 2);
   const int blocks = (rows + per - 1) / per;
   if (head_dim == 128)
     hipLaunchKernelGGL((merge_kernel<128>), dim3(blocks), dim3(kThreads), 0, stream, p);
@@ -889,16 +1179,16 @@ hipError_t launch_merge(const MergeParams& p, int head_dim, hipStream_t stream) 
   return hipGetLastError();
 }
 
-hipError_t launch_attn_units(const AttnParams& p, int num_units, int head_dim, int kv_kind, hipStream_t stream) {
-  if (num_units <= 0) return hipSuccess;
+hipError_t launch_attn(const AttnParams& p, int grid, int head_dim, int kv_kind, hipStream_t stream) {
+  if (grid <= 0) return hipSuccess;
   if (head_dim == 128) {
-    if (kv_kind == kKvBf16) return launch_attn_t<128, kKvBf16>(p, num_units, stream);
-    if (kv_kind == kKvFp8) return launch_attn_t<128, kKvFp8>(p, num_units, stream);
-    return launch_attn_t<128, kKvF32>(p, num_units, stream);
+    if (kv_kind == kKvBf16) return launch_attn_t<128, kKvBf16>(p, grid, stream);
+    if (kv_kind == kKvFp8) return launch_attn_t<128, kKvFp8>(p, grid, stream);
+    return launch_attn_t<128, kKvF32>(p, grid, stream);
   }
-  if (kv_kind == kKvBf16) return launch_attn_t<64, kKvBf16>(p, num_units, stream);
-  if (kv_kind == kKvFp8) return launch_attn_t<64, kKvFp8>(p, num_units, stream);
-  return launch_attn_t<64, kKvF32>(p, num_units, stream);
+  if (kv_kind == kKvBf16) return launch_attn_t<64, kKvBf16>(p, grid, stream);
+  if (kv_kind == kKvFp8) return launch_attn_t<64, kKvFp8>(p, grid, stream);
+  return launch_attn_t<64, kKvF32>(p, grid, stream);
 }
 
 }  // namespace tts
@@ -906,11 +1196,11 @@ hipError_t launch_attn_units(const AttnParams& p, int num_units, int head_dim, i
 #ifdef TTS_PROFILE_UNITS
 extern "C" int tts_prof_read(uint64_t* host, int n) {
   if (n > tts::kProfSlots) n = tts::kProfSlots;
-  return static_cast<int>(hipMemcpyFromSymbol(host, HIP_SYMBOL(tts::g_prof), sizeof(uint64_t) * 4 * n, 0,
+  return static_cast<int>(hipMemcpyFromSymbol(host, HIP_SYMBOL(tts::g_prof), sizeof(uint64_t) * 8 * n, 0,
                                               hipMemcpyDeviceToHost));
 }
 extern "C" int tts_prof_clear() {
-  static uint64_t zeros[tts::kProfSlots][4];
+  static uint64_t zeros[tts::kProfSlots][8];
   return static_cast<int>(hipMemcpyToSymbol(HIP_SYMBOL(tts::g_prof), zeros, sizeof(zeros), 0, hipMemcpyHostToDevice));
 }
 #endif

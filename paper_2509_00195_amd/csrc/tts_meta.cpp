@@ -89,6 +89,7 @@ int build_host_meta(const MetaInput& in, HostMeta* out, std::string* err) {
   m.tables.assign(in.block_tables, in.block_tables + static_cast<size_t>(S) * mb);
   m.seq_lens.assign(in.seq_lens, in.seq_lens + S);
   m.tail_lblock.assign(S, 0);
+  m.req_off.assign(in.req_seq_offsets, in.req_seq_offsets + in.num_reqs + 1);
   m.perm.reserve(S);
   m.path_seg_off.assign(S + 1, 0);
   std::vector<std::vector<int32_t>> beam_segs(S);
@@ -234,124 +235,5 @@ int64_t coverage_rows(const HostMeta& m, const int32_t* seq_lens, int32_t* rows,
   return n;
 }
 
-namespace {
-// Blocks per workgroup a segment piece or a tail split aims for. A piece
-// emits one partial state per covered row, so pieces stay long enough that
-// the partial bytes stay well below the KV bytes they summarise.
-#ifndef TTS_SEG_PIECE_BLOCKS
-#define TTS_SEG_PIECE_BLOCKS 32
-#endif
-#ifndef TTS_TAIL_SPLIT_BLOCKS
-#define TTS_TAIL_SPLIT_BLOCKS 32
-#endif
-constexpr int32_t kSegPieceBlocks = TTS_SEG_PIECE_BLOCKS;
-constexpr int32_t kTailSplitBlocks = TTS_TAIL_SPLIT_BLOCKS;
-// Workgroups are dispatched to the 8 XCDs of an MI355X round-robin by
-// workgroup id; each XCD has its own L2.
-constexpr int kXcds = 8;
-
-// Relative time of a unit: blocks, divided among the waves that split them.
-int64_t unit_cost(int32_t nblk, int32_t nrows) {
-  const int32_t nrt = (nrows + 15) / 16;
-  const int32_t wt = nrt >= 3 ? 1 : (nrt == 2 ? 2 : 4);
-  return static_cast<int64_t>(nblk) * (4 + 8 / wt);
-}
-}  // namespace
-
-void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) {
-  const int32_t S = m.num_seqs;
-  const int32_t g = shape.num_q_heads / shape.num_kv_heads;
-  const int32_t rpu = (kRowsPerUnit / g) * g;  // rows per unit, whole beams
-  const int32_t nseg = static_cast<int32_t>(m.seg_req.size());
-  WorkPlan& p = *plan;
-  p = WorkPlan();
-
-  // Segment pieces (whole block pairs) and their slots; slot order along a
-  // beam's path is the merge order (segments root to leaf, then the tail).
-  std::vector<int32_t> pieces(nseg), slot0(nseg), blk_off(nseg);
-  for (int32_t s = 0; s < nseg; ++s) {
-    pieces[s] = std::max(1, (m.seg_nblocks[s] + kSegPieceBlocks / 2) / kSegPieceBlocks);
-    const int32_t par = m.seg_parent[s];
-    slot0[s] = par < 0 ? 0 : slot0[par] + pieces[par];  // parents precede children (preorder)
-    blk_off[s] = static_cast<int32_t>(p.seg_blocks.size());
-    const int32_t beam = m.perm[m.seg_beam_begin[s]];
-    const int32_t* row = m.tables.data() + static_cast<size_t>(beam) * m.max_blocks;
-    p.seg_blocks.insert(p.seg_blocks.end(), row + m.seg_lblock_begin[s],
-                        row + m.seg_lblock_begin[s] + m.seg_nblocks[s]);
-  }
-
-  // Groups of units that read the same blocks (all row blocks of one piece
-  // and KV head) go to the same XCD so that the blocks come from its L2.
-  struct Group {
-    int64_t cost;
-    std::vector<Unit> units;
-  };
-  std::vector<Group> groups;
-  for (int32_t s = 0; s < nseg; ++s) {
-    const int32_t G = m.seg_beam_end[s] - m.seg_beam_begin[s];
-    const int32_t R = G * g;
-    const int32_t n = m.seg_nblocks[s];
-    const int32_t npairs = (n + 1) / 2;
-    for (int32_t j = 0; j < pieces[s]; ++j) {
-      const int32_t a = 2 * static_cast<int32_t>(static_cast<int64_t>(npairs) * j / pieces[s]);
-      const int32_t e = std::min(n, 2 * static_cast<int32_t>(static_cast<int64_t>(npairs) * (j + 1) / pieces[s]));
-      for (int32_t kvh = 0; kvh < shape.num_kv_heads; ++kvh) {
-        Group gr{0, {}};
-        for (int32_t row0 = 0; row0 < R; row0 += rpu) {
-          const int32_t nrows = std::min(rpu, R - row0);
-          gr.units.push_back(Unit{kvh, kSegmentPiece, m.seg_beam_begin[s], G, row0, nrows, blk_off[s] + a, e - a,
-                                  slot0[s] + j, 0, 0, 0});
-          gr.cost += unit_cost(e - a, nrows);
-        }
-        groups.push_back(std::move(gr));
-      }
-    }
-  }
-  p.slot_base.assign(S + 1, 0);
-  p.tail_nsplit.assign(S, 1);
-  for (int32_t b = 0; b < S; ++b) {
-    int32_t tail_slot0 = 0;
-    const int32_t nseg_b = m.path_seg_off[b + 1] - m.path_seg_off[b];
-    if (nseg_b > 0) {
-      const int32_t deepest = m.path_seg[m.path_seg_off[b + 1] - 1];
-      tail_slot0 = slot0[deepest] + pieces[deepest];
-    }
-    const int32_t nblk = (m.seq_lens[b] + m.block_size - 1) / m.block_size;
-    const int32_t tb = std::max(0, nblk - m.tail_lblock[b]);
-    p.tail_nsplit[b] = std::max(1, (tb + kTailSplitBlocks / 2) / kTailSplitBlocks);
-    p.slot_base[b + 1] = p.slot_base[b] + tail_slot0 + p.tail_nsplit[b];
-    const int32_t per = 2 * (((tb + 1) / 2 + p.tail_nsplit[b] - 1) / p.tail_nsplit[b]);
-    for (int32_t kvh = 0; kvh < shape.num_kv_heads; ++kvh) {
-      for (int32_t j = 0; j < p.tail_nsplit[b]; ++j) {
-        Unit u{kvh, kTailSplit, m.pos_of[b], 1, 0, g, j, p.tail_nsplit[b], tail_slot0 + j, 0, 0, 0};
-        groups.push_back(Group{unit_cost(std::max(1, std::min(per, tb)), g), {u}});
-      }
-    }
-  }
-  p.num_slots = p.slot_base[S];
-
-  // Longest-processing-time assignment of groups to XCDs, then each XCD's
-  // units longest first; unit i runs on XCD i % 8, so the per-XCD lists are
-  // interleaved and the shorter ones padded with empty units.
-  std::stable_sort(groups.begin(), groups.end(), [](const Group& a, const Group& b) { return a.cost > b.cost; });
-  std::vector<int64_t> load(kXcds, 0);
-  std::vector<std::vector<std::pair<int64_t, Unit>>> xq(kXcds);
-  for (const Group& gr : groups) {
-    int x = 0;
-    for (int k = 1; k < kXcds; ++k)
-      if (load[k] < load[x]) x = k;
-    load[x] += gr.cost;
-    for (const Unit& u : gr.units) xq[x].push_back({unit_cost(u.nblk, u.nrows), u});
-  }
-  size_t longest = 0;
-  for (auto& q : xq) {
-    std::stable_sort(q.begin(), q.end(), [](const auto& a, const auto& b) { return a.first > b.first; });
-    longest = std::max(longest, q.size());
-  }
-  const Unit pad{0, kTailSplit, 0, 0, 0, 0, 0, 1, 0, 0, 0, 0};
-  p.units.reserve(longest * kXcds);
-  for (size_t i = 0; i < longest; ++i)
-    for (int x = 0; x < kXcds; ++x) p.units.push_back(i < xq[x].size() ? xq[x][i].second : pad);
-}
 
 }  // namespace tts

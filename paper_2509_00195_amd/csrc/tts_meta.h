@@ -44,6 +44,7 @@ struct HostMeta {
   // build-time copies
   std::vector<int32_t> tables, seq_lens;
   std::vector<int32_t> pos_of;  // original beam -> position
+  std::vector<int32_t> req_off; // [num_reqs + 1] request offsets (positions of a request are contiguous)
 };
 
 // Validates the input and builds the canonical metadata. Returns 0 on
@@ -55,17 +56,25 @@ int build_host_meta(const MetaInput& in, HostMeta* out, std::string* err);
 // writes at most cap rows.
 int64_t coverage_rows(const HostMeta& m, const int32_t* seq_lens, int32_t* rows, int64_t cap);
 
-// Kernel work list for one attention shape.
+// Kernel work list for one attention shape (see build_work_plan).
 struct WorkPlan {
-  std::vector<Unit> units;
-  std::vector<int32_t> seg_blocks;  // physical ids of every segment piece
-  std::vector<int32_t> slot_base;   // [S + 1] by original beam
-  std::vector<int32_t> tail_nsplit; // by original beam
-  int64_t num_slots = 0;
+  std::vector<UnitRec> recs;      // record k < num_bins: workgroup k's first unit
+  std::vector<int32_t> slot_off;  // [S + 1] by original beam: CSR into slot_rows
+  std::vector<int32_t> slot_rows; // partial row of the beam's row 0 (KV head 0), merge order
+  // The same lists as a dense table for the merge kernel: beam b's row
+  // holds its slot count, then its slots; slot_stride ints per beam.
+  std::vector<int32_t> slot_tab;
+  int32_t slot_stride = 0;
+  std::vector<int32_t> build_len; // [S] lengths the plan was built for
+  int32_t rows_per_head = 0;      // partial rows per KV head
+  int32_t num_bins = 0;
+  int64_t num_units = 0;          // records with work
+  int64_t num_slots = 0;          // slot_rows.size()
 };
 
 struct PlanShape {
   int32_t num_q_heads, num_kv_heads, head_dim, kv_bytes;
+  int32_t num_bins;  // persistent workgroups (one per compute unit)
 };
 
 void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan);

@@ -1,0 +1,442 @@
+// Kernel work list of the prefix-shared decode attention.
+//
+// The attention kernel runs one persistent workgroup per compute unit; each
+// workgroup walks a chain of unit records. A unit is a set of query rows
+// (whole beams, consecutive in the canonical order, one KV head) and a list
+// of KV blocks, each applying to a contiguous range of those rows. Two kinds
+// of unit cover every (beam, used block) exactly once per KV head:
+//
+// * Wide units. A segment shared by more beams than fit in a narrow unit
+//   (its rows exceed kMaxRows) is cut into row chunks of whole beams (up to
+//   kMaxWideRows rows: the four waves of the workgroup share every block
+//   through LDS, each taking a quarter of the row tiles) and, along its
+//   blocks, into pieces; every (piece, chunk) is a unit whose blocks apply
+//   to all of its rows. (fp32 and fp8 caches use chunks of kMaxRows rows.) The
+//   chunks of one piece read the same blocks and are placed on one XCD.
+// * Narrow units. Everything else -- segments of few beams and every beam's
+//   private tail -- is listed depth-first over the prefix tree (a segment's
+//   blocks, then its subtrees and the tails of the beams ending at it, in
+//   canonical order). Consecutive entries of that list always cover a
+//   contiguous range of beams, so the list is cut into units of at most
+//   kMaxUnitBeams beams / kMaxRows rows / kMaxEntries entries and about
+//   equal cost: a small subtree with its tails becomes one unit and one
+//   partial state per beam instead of one per segment.
+//
+// Units are replicated per KV head, grouped, spread over the XCDs longest
+// first and then over each XCD's workgroups longest first.
+#include <algorithm>
+#include <cmath>
+#include <numeric>
+
+#include "tts_meta.h"
+
+namespace tts {
+namespace {
+
+// Cost model (microseconds of one workgroup). A unit streams its KV blocks,
+// its query rows and its partial states (written here, read again by the
+// merge) through the compute unit's share of memory bandwidth, and runs
+// the matrix work of its row tiles x block pairs on four SIMDs; the two
+// overlap, plus a fixed part (record, barriers, combine).
+constexpr double kBytesPerUs = 5.0e6 / 256;  // ~5 TB/s over 256 compute units
+constexpr double kTilePairUs = 350.0 / 2400.0;  // one 16-row tile x one block pair, 2.4 GHz
+constexpr double kUnitFixedUs = 0.8;
+#ifndef TTS_UNITS_PER_BIN
+#define TTS_UNITS_PER_BIN 0.5
+#endif
+constexpr double kUnitsPerBin = TTS_UNITS_PER_BIN;
+constexpr double kMinUnitUs = 3.0;
+constexpr int kXcds = 8;  // workgroup k of a launch runs on XCD k % 8
+
+int tiles_of(int rows) { return (rows + 15) / 16; }
+
+struct CostModel {
+  double blk_bytes, q_row_bytes, part_row_bytes;
+  double mem_us(double blocks, int rows) const {
+    return (blocks * blk_bytes + rows * (q_row_bytes + part_row_bytes)) / kBytesPerUs;
+  }
+  // Narrow units: the waves split the block pairs, every wave runs every tile.
+  double narrow_us(int blocks, int rows) const {
+    const double comp = tiles_of(rows) * ((blocks + 1) / 2) * kTilePairUs / 4.0;
+    return std::max(mem_us(blocks, rows), comp) + kUnitFixedUs;
+  }
+  // Wide units: every wave runs every pair on its quarter of the tiles.
+  double wide_us(int blocks, int rows) const {
+    const double comp = ((tiles_of(rows) + 3) / 4) * ((blocks + 1) / 2) * kTilePairUs;
+    return std::max(mem_us(blocks, rows), comp) + kUnitFixedUs;
+  }
+  double bytes(int blocks, int rows) const { return mem_us(blocks, rows) * kBytesPerUs; }
+};
+
+struct Tmpl {
+  int32_t lo = 0, hi = 0;  // beam positions [lo, hi)
+  int32_t mode = kModeNarrow;
+  std::vector<int32_t> ids;
+  std::vector<uint32_t> info;
+  int32_t nstatic = 0;
+  double cost = 0;
+  int32_t group = -1;  // wide units: index of their piece
+};
+
+struct NItem {
+  int32_t id;
+  int32_t p0, p1;
+  int32_t valid;
+  uint32_t flags;
+  double cost;
+};
+
+}  // namespace
+
+void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) {
+  WorkPlan& P = *plan;
+  P = WorkPlan();
+  const int32_t S = m.num_seqs;
+  const int32_t g = shape.num_q_heads / shape.num_kv_heads;
+  const int32_t hkv = shape.num_kv_heads;
+  const int32_t bs = m.block_size;
+  const int32_t RB = std::max(1, std::min(kMaxUnitBeams, kMaxRows / g));  // beams per narrow unit
+  // Beams per wide unit (bf16 caches; fp32 and fp8 caches use narrow-sized chunks).
+  const bool wide_mode = shape.kv_bytes == 2;
+  const int32_t RW = wide_mode ? std::max(1, std::min(kMaxWideBeams, kMaxWideRows / g)) : RB;
+  const int32_t nseg = static_cast<int32_t>(m.seg_req.size());
+  const int32_t nbins = std::max(1, shape.num_bins);
+  P.num_bins = nbins;
+  P.build_len.assign(m.seq_lens.begin(), m.seq_lens.end());
+
+  CostModel cm;
+  cm.blk_bytes = 2.0 * bs * shape.head_dim * shape.kv_bytes;
+  cm.q_row_bytes = shape.head_dim * (shape.kv_bytes == 4 ? 4.0 : 2.0);
+  cm.part_row_bytes = 2.0 * (shape.head_dim + 2) * 4.0;
+  const double blk_us = cm.blk_bytes / kBytesPerUs;
+
+  // ---- tree structure ----------------------------------------------------
+  std::vector<std::vector<int32_t>> children(nseg), leaves(nseg);
+  std::vector<std::vector<std::pair<int32_t, int32_t>>> top(std::max<size_t>(1, m.req_off.size()) - 1);
+  auto req_of_pos = [&](int32_t pos) {
+    return static_cast<int32_t>(std::upper_bound(m.req_off.begin(), m.req_off.end(), pos) - m.req_off.begin()) - 1;
+  };
+  for (int32_t s = 0; s < nseg; ++s) {
+    if (m.seg_parent[s] >= 0)
+      children[m.seg_parent[s]].push_back(s);
+    else
+      top[m.seg_req[s]].push_back({m.seg_beam_begin[s], s});
+  }
+  for (int32_t pos = 0; pos < S; ++pos) {
+    const int32_t b = m.perm[pos];
+    const int32_t k0 = m.path_seg_off[b], k1 = m.path_seg_off[b + 1];
+    if (k1 > k0)
+      leaves[m.path_seg[k1 - 1]].push_back(pos);
+    else
+      top[req_of_pos(pos)].push_back({pos, -1 - pos});
+  }
+  std::vector<char> wide(nseg, 0);
+  for (int32_t s = 0; s < nseg; ++s) wide[s] = (m.seg_beam_end[s] - m.seg_beam_begin[s]) > RB;
+  auto seg_block = [&](int32_t s, int32_t j) {
+    const int32_t b = m.perm[m.seg_beam_begin[s]];
+    return m.tables[static_cast<size_t>(b) * m.max_blocks + m.seg_lblock_begin[s] + j];
+  };
+
+  // ---- depth-first list of the narrow work --------------------------------
+  std::vector<NItem> items;
+  auto emit_tail = [&](int32_t pos) {
+    const int32_t b = m.perm[pos];
+    const int32_t L = m.seq_lens[b];
+    const int32_t nb = (L + bs - 1) / bs;
+    for (int32_t j = m.tail_lblock[b]; j < nb; ++j) {
+      const int32_t v = std::min(bs, L - j * bs);
+      const uint32_t fl = (j == nb - 1 && v < bs) ? kEntLive : 0u;
+      items.push_back({m.tables[static_cast<size_t>(b) * m.max_blocks + j], pos, pos + 1, v, fl, blk_us});
+    }
+    items.push_back({0, pos, pos + 1, 1, kEntExt, 0.0});
+  };
+  // Iterative walk: a stack of (segment, or -1 - leaf position).
+  std::vector<int32_t> stack;
+  auto push_sorted = [&](std::vector<std::pair<int32_t, int32_t>>& v) {
+    std::sort(v.begin(), v.end());
+    for (auto it = v.rbegin(); it != v.rend(); ++it) stack.push_back(it->second);
+  };
+  std::vector<std::pair<int32_t, int32_t>> tmp;
+  for (auto& t : top) {
+    push_sorted(t);
+    while (!stack.empty()) {
+      const int32_t x = stack.back();
+      stack.pop_back();
+      if (x < 0) {
+        emit_tail(-1 - x);
+        continue;
+      }
+      const int32_t bb = m.seg_beam_begin[x], be = m.seg_beam_end[x];
+      if (!wide[x]) {
+        for (int32_t j = 0; j < m.seg_nblocks[x]; ++j)
+          items.push_back({seg_block(x, j), bb, be, bs, 0u, blk_us});
+      }
+      tmp.clear();
+      for (int32_t c : children[x]) tmp.push_back({m.seg_beam_begin[c], c});
+      for (int32_t pos : leaves[x]) tmp.push_back({pos, -1 - pos});
+      push_sorted(tmp);
+    }
+  }
+
+  // ---- target unit time ---------------------------------------------------
+  // Lower bound of the work per KV head: every block read once, every tile
+  // pair computed once, spread evenly.
+  double total = 0;
+  for (const NItem& it : items) total += it.cost;
+  for (int32_t s = 0; s < nseg; ++s) {
+    if (!wide[s]) continue;
+    const int32_t G = m.seg_beam_end[s] - m.seg_beam_begin[s];
+    total += std::max(m.seg_nblocks[s] * blk_us, tiles_of(G * g) * ((m.seg_nblocks[s] + 1) / 2) * kTilePairUs / 4.0);
+  }
+  const double T = std::max(kMinUnitUs, total * hkv / (nbins * kUnitsPerBin));
+
+  // ---- templates (one per unit, before replication over KV heads) --------
+  // A wide segment of G beams and n blocks is cut into C row chunks and P
+  // pieces, in the wide mode (chunks of up to RW beams) or the narrow mode
+  // (up to RB beams): the choice that moves the fewest bytes among those
+  // whose units fit the target time (else the fastest).
+  std::vector<Tmpl> tm;
+  int32_t ngroups = 0;
+  for (int32_t s = 0; s < nseg; ++s) {  // preorder: ancestors first
+    if (!wide[s]) continue;
+    const int32_t bb = m.seg_beam_begin[s], G = m.seg_beam_end[s] - bb;
+    const int32_t n = m.seg_nblocks[s], np = (n + 1) / 2;
+    struct Choice {
+      int32_t mode, C, P;
+      double bytes, us;
+    } best{kModeNarrow, 0, 0, 0, 0};
+    bool have = false, best_fits = false;
+    for (int32_t mode : {kModeWide, kModeNarrow}) {
+      if (mode == kModeWide && !wide_mode) continue;
+      const int32_t cap = mode == kModeWide ? RW : RB;
+      for (int32_t C = (G + cap - 1) / cap; C <= std::min(G, 4 * ((G + cap - 1) / cap)); ++C) {
+        const int32_t rows = ((G + C - 1) / C) * g;
+        for (int32_t P = std::max(1, (n + kMaxEntries - 1) / kMaxEntries); P <= np; ++P) {
+          const int32_t blocks = std::min(n, 2 * ((np + P - 1) / P));
+          const double us = mode == kModeWide ? cm.wide_us(blocks, rows) : cm.narrow_us(blocks, rows);
+          const double bytes = static_cast<double>(C) * P * cm.bytes(blocks, rows);
+          const bool fits = us <= T;
+          const bool better = !have || (fits && !best_fits) ||
+                              (fits == best_fits && (fits ? bytes < best.bytes : us < best.us));
+          if (better) {
+            best = {mode, C, P, bytes, us};
+            best_fits = fits;
+            have = true;
+          }
+          if (fits) break;  // more pieces only add bytes
+        }
+      }
+    }
+    const int32_t C = best.C, pieces = best.P;
+    for (int32_t j = 0; j < pieces; ++j) {
+      const int32_t a = 2 * static_cast<int32_t>(static_cast<int64_t>(np) * j / pieces);
+      const int32_t e = std::min(n, 2 * static_cast<int32_t>(static_cast<int64_t>(np) * (j + 1) / pieces));
+      for (int32_t c = 0; c < C; ++c) {
+        Tmpl t;
+        t.lo = bb + static_cast<int32_t>(static_cast<int64_t>(G) * c / C);
+        t.hi = bb + static_cast<int32_t>(static_cast<int64_t>(G) * (c + 1) / C);
+        const int32_t rows = (t.hi - t.lo) * g;
+        t.mode = best.mode;
+        for (int32_t k = a; k < e; ++k) {
+          t.ids.push_back(seg_block(s, k));
+          t.info.push_back(t.mode == kModeWide ? 0u : ent_info(0, rows, bs, 0u));
+        }
+        t.nstatic = e - a;
+        t.cost = t.mode == kModeWide ? cm.wide_us(e - a, rows) : cm.narrow_us(e - a, rows);
+        t.group = ngroups;
+        tm.push_back(std::move(t));
+      }
+      ++ngroups;
+    }
+  }
+  {
+    Tmpl cur;
+    std::vector<NItem> ext;
+    bool open = false;
+    auto flush = [&]() {
+      if (!open) return;
+      for (const NItem& it : ext) {
+        cur.ids.push_back(it.p0 - cur.lo);
+        cur.info.push_back(ent_info((it.p0 - cur.lo) * g, (it.p1 - cur.lo) * g, 1, kEntExt));
+      }
+      cur.cost = cm.narrow_us(cur.nstatic, (cur.hi - cur.lo) * g);
+      tm.push_back(std::move(cur));
+      cur = Tmpl();
+      ext.clear();
+      open = false;
+    };
+    std::vector<NItem> pend;  // static items of the open unit (row offsets fixed at flush)
+    auto flush_all = [&]() {
+      if (!open) return;
+      for (const NItem& it : pend) {
+        cur.ids.push_back(it.id);
+        cur.info.push_back(ent_info((it.p0 - cur.lo) * g, (it.p1 - cur.lo) * g, it.valid, it.flags));
+      }
+      cur.nstatic = static_cast<int32_t>(pend.size());
+      pend.clear();
+      flush();
+    };
+    for (const NItem& it : items) {
+      if (open) {
+        const int32_t lo = std::min(cur.lo, it.p0), hi = std::max(cur.hi, it.p1);
+        const bool fits = hi - lo <= RB && static_cast<int32_t>(pend.size() + ext.size()) + 1 <= kMaxEntries &&
+                          cur.cost + it.cost + cm.mem_us(0, (hi - lo) * g) + kUnitFixedUs <= T;
+        if (!fits) flush_all();
+      }
+      if (!open) {
+        open = true;
+        cur.lo = it.p0;
+        cur.hi = it.p1;
+      }
+      cur.lo = std::min(cur.lo, it.p0);
+      cur.hi = std::max(cur.hi, it.p1);
+      cur.cost += it.cost;
+      if (it.flags & kEntExt)
+        ext.push_back(it);
+      else
+        pend.push_back(it);
+    }
+    flush_all();
+  }
+
+  // ---- partial rows and merge lists ----------------------------------------
+  std::vector<int32_t> prow0(tm.size());
+  std::vector<std::vector<int32_t>> per_beam(S);
+  int32_t rows = 0;
+  for (size_t t = 0; t < tm.size(); ++t) {
+    prow0[t] = rows;
+    const int32_t nb = tm[t].hi - tm[t].lo;
+    std::vector<char> touched(nb, tm[t].mode == kModeWide ? 1 : 0);
+    for (size_t k = 0; tm[t].mode == kModeNarrow && k < tm[t].ids.size(); ++k) {
+      const uint32_t inf = tm[t].info[k];
+      const int32_t r0 = inf & 63, r1 = ((inf >> 6) & 63) + 1;
+      for (int32_t i = r0 / g; i < (r1 + g - 1) / g && i < nb; ++i) touched[i] = 1;
+    }
+    for (int32_t i = 0; i < nb; ++i)
+      if (touched[i]) per_beam[m.perm[tm[t].lo + i]].push_back(rows + i * g);
+    rows += nb * g;
+  }
+  P.rows_per_head = rows;
+  P.slot_off.assign(S + 1, 0);
+  for (int32_t b = 0; b < S; ++b) P.slot_off[b + 1] = P.slot_off[b] + static_cast<int32_t>(per_beam[b].size());
+  P.slot_rows.reserve(P.slot_off[S]);
+  for (int32_t b = 0; b < S; ++b) P.slot_rows.insert(P.slot_rows.end(), per_beam[b].begin(), per_beam[b].end());
+  P.num_slots = static_cast<int64_t>(P.slot_rows.size());
+  size_t most = 0;
+  for (const auto& v : per_beam) most = std::max(most, v.size());
+  P.slot_stride = std::max<int32_t>(kMergeBatch + 1, static_cast<int32_t>((most + 1 + 15) / 16 * 16));
+  P.slot_tab.assign(static_cast<size_t>(S) * P.slot_stride, 0);
+  for (int32_t b = 0; b < S; ++b) {
+    int32_t* row = P.slot_tab.data() + static_cast<size_t>(b) * P.slot_stride;
+    row[0] = static_cast<int32_t>(per_beam[b].size());
+    std::copy(per_beam[b].begin(), per_beam[b].end(), row + 1);
+  }
+
+  // ---- placement: groups -> XCDs -> workgroups ------------------------------
+  struct Work {
+    int32_t t, kvh;
+    double cost;
+  };
+  struct Group {
+    double cost = 0;
+    int32_t first = 0;  // creation order of its first unit (wide before narrow)
+    std::vector<Work> units;
+  };
+  std::vector<Group> groups;
+  {
+    std::vector<int32_t> gidx(static_cast<size_t>(ngroups) * hkv, -1);
+    for (int32_t kvh = 0; kvh < hkv; ++kvh) {
+      for (size_t t = 0; t < tm.size(); ++t) {
+        int32_t gi;
+        if (tm[t].group >= 0) {
+          int32_t& slot = gidx[static_cast<size_t>(tm[t].group) * hkv + kvh];
+          if (slot < 0) {
+            slot = static_cast<int32_t>(groups.size());
+            groups.emplace_back();
+            groups.back().first = static_cast<int32_t>(t);
+          }
+          gi = slot;
+        } else {
+          gi = static_cast<int32_t>(groups.size());
+          groups.emplace_back();
+          groups.back().first = static_cast<int32_t>(t);
+        }
+        groups[gi].units.push_back({static_cast<int32_t>(t), kvh, tm[t].cost});
+        groups[gi].cost += tm[t].cost;
+      }
+    }
+  }
+  std::vector<int32_t> gorder(groups.size());
+  std::iota(gorder.begin(), gorder.end(), 0);
+  std::stable_sort(gorder.begin(), gorder.end(), [&](int32_t a, int32_t b) { return groups[a].cost > groups[b].cost; });
+  const int32_t nx = std::min(kXcds, nbins);
+  std::vector<int32_t> xbins(nx, 0);
+  for (int32_t k = 0; k < nbins; ++k) xbins[k % nx]++;
+  std::vector<double> xload(nx, 0);
+  std::vector<std::vector<Work>> xunits(nx);
+  for (int32_t gi : gorder) {
+    int32_t x = 0;
+    for (int32_t k = 1; k < nx; ++k)
+      if (xload[k] / xbins[k] < xload[x] / xbins[x]) x = k;
+    xload[x] += groups[gi].cost;
+    for (const Work& w : groups[gi].units) xunits[x].push_back(w);
+  }
+  std::vector<std::vector<Work>> bins(nbins);
+  for (int32_t x = 0; x < nx; ++x) {
+    auto& v = xunits[x];
+    std::stable_sort(v.begin(), v.end(), [](const Work& a, const Work& b) { return a.cost > b.cost; });
+    std::vector<int32_t> mine;
+    for (int32_t k = x; k < nbins; k += nx) mine.push_back(k);
+    std::vector<double> load(mine.size(), 0);
+    for (const Work& w : v) {
+      size_t best = 0;
+      for (size_t k = 1; k < mine.size(); ++k)
+        if (load[k] < load[best]) best = k;
+      load[best] += w.cost;
+      bins[mine[best]].push_back(w);
+    }
+  }
+  // Within a workgroup, wide units first (their chunks run concurrently on
+  // the XCD's other workgroups and share its L2), then in creation order.
+  for (auto& v : bins)
+    std::stable_sort(v.begin(), v.end(), [](const Work& a, const Work& b) { return a.t < b.t; });
+
+  // ---- records ---------------------------------------------------------------
+  auto make_rec = [&](const Work& w) {
+    UnitRec r{};
+    const Tmpl& t = tm[w.t];
+    r.kvh = w.kvh;
+    r.nrows = (t.hi - t.lo) * g;
+    r.nstatic = t.nstatic;
+    r.nent = static_cast<int32_t>(t.ids.size());
+    r.prow0 = prow0[w.t];
+    r.next = -1;
+    r.mode = t.mode;
+    for (int32_t i = 0; i < t.hi - t.lo; ++i) r.beams[i] = m.perm[t.lo + i];
+    for (size_t k = 0; k < t.ids.size(); ++k) {
+      r.ent_id[k] = t.ids[k];
+      r.ent_info[k] = t.info[k];
+    }
+    return r;
+  };
+  P.recs.assign(nbins, UnitRec{});
+  for (int32_t k = 0; k < nbins; ++k) P.recs[k].next = -1;
+  for (int32_t k = 0; k < nbins; ++k) {
+    int32_t prev = -1;
+    for (size_t i = 0; i < bins[k].size(); ++i) {
+      int32_t idx;
+      if (i == 0) {
+        idx = k;
+        P.recs[k] = make_rec(bins[k][i]);
+      } else {
+        idx = static_cast<int32_t>(P.recs.size());
+        P.recs.push_back(make_rec(bins[k][i]));
+      }
+      if (prev >= 0) P.recs[prev].next = idx;
+      prev = idx;
+      P.num_units++;
+    }
+  }
+}
+
+}  // namespace tts

@@ -1,5 +1,5 @@
-// Work-unit and kernel-parameter layouts shared by the host planner and the
-// HIP kernels. Plain C++ (no HIP types) so the planner builds with any
+// Work-unit records and kernel parameters shared by the host planner and
+// the HIP kernels. Plain C++ (no HIP types) so the planner builds with any
 // host compiler.
 #pragma once
 
@@ -7,38 +7,60 @@
 
 namespace tts {
 
-// Rows of one KV head handled by one workgroup: 4 waves x 16 rows, cut at
-// whole beams (a unit covers floor(64 / g) beams).
-constexpr int kRowsPerUnit = 64;
-constexpr int kUnitInts = 12;
+// One workgroup handles at most this many query rows of one KV head
+// (4 row tiles of 16); a row is one (beam, query head of the KV group).
+constexpr int kMaxRows = 64;
+// Block entries per unit (one per lane of a wave).
+constexpr int kMaxEntries = 64;
+// Beams per unit.
+constexpr int kMaxUnitBeams = 16;
 
-enum UnitKind : int32_t { kSegmentPiece = 0, kTailSplit = 1 };
+// Entry info word: rows [r0, r1) of the unit that attend to the block, and
+// its valid token count (static; see the flags). Wide units' blocks apply
+// to all of their rows and are full; their info words are not read.
+//   bits  0..5   r0
+//   bits  6..11  r1 - 1
+//   bits 12..15  valid - 1
+//   bit  16      kEntLive: the beam's partially filled last block at build
+//                time; valid grows with the beam's live length
+//   bit  17      kEntExt: not a block; the beam (id = its slot in the unit)
+//                may have grown past its build-time blocks, which are then
+//                read from the live block table
+constexpr uint32_t kEntLive = 1u << 16;
+constexpr uint32_t kEntExt = 1u << 17;
 
-// One workgroup's share of the decode step: query rows of one KV head
-// against one contiguous run of KV blocks.
-//
-// Rows: the beams at positions [pos0, pos0 + nbeams) of the canonical order
-// each contribute g = Hq/Hkv rows (beam-major, then query head); the unit
-// owns rows [row0, row0 + nrows) of those nbeams * g.
-// Blocks: a segment piece reads seg_blocks[blk_off .. blk_off + nblk), all
-// full; a tail split reads split blk_off of nblk equal parts of the beam's
-// private blocks [tail_lblock, ceil(seq_len / block_size)), from the live
-// block table (last block possibly partial).
-// Output: a partial softmax state written to slot `slot` of every covered
-// beam (slot order = merge order). A unit with nrows == 0 is padding.
-struct Unit {
+inline constexpr uint32_t ent_info(int r0, int r1, int valid, uint32_t flags) {
+  return static_cast<uint32_t>(r0) | (static_cast<uint32_t>(r1 - 1) << 6) |
+         (static_cast<uint32_t>(valid - 1) << 12) | flags;
+}
+
+// Wide units (kModeWide): up to kMaxWideRows rows of one segment piece;
+// each of the 4 waves owns a quarter of the row tiles (at most 3) and
+// every block applies to every row.
+constexpr int kMaxWideRows = 192;
+constexpr int kMaxWideBeams = 64;
+enum UnitMode : int32_t { kModeNarrow = 0, kModeWide = 1 };
+
+// One unit of work: query rows of up to kMaxUnitBeams beams (kMaxWideBeams
+// for a wide unit), consecutive in the canonical order, for one KV head,
+// against a list of KV blocks, each applying to a contiguous range of those
+// rows. Rows are beam-major: row r belongs to the unit's beam r / g and
+// query head kvh * g + r % g. The unit writes one partial softmax state per
+// row to partial row kvh * rows_per_head + prow0 + r.
+struct UnitRec {
   int32_t kvh;
-  int32_t kind;
-  int32_t pos0;
-  int32_t nbeams;
-  int32_t row0;
-  int32_t nrows;
-  int32_t blk_off;
-  int32_t nblk;
-  int32_t slot;
-  int32_t pad0, pad1, pad2;
+  int32_t nrows;    // 0: nothing to do (an idle workgroup)
+  int32_t nstatic;  // block entries (pairs are entries 2i, 2i+1)
+  int32_t nent;     // block entries + extension entries (these come last)
+  int32_t prow0;
+  int32_t next;     // next record of the same workgroup, -1 at the end
+  int32_t mode;     // UnitMode
+  int32_t pad1;
+  int32_t beams[kMaxWideBeams];  // original beam index of each unit beam
+  int32_t ent_id[kMaxEntries];   // physical block id (extension: beam slot)
+  uint32_t ent_info[kMaxEntries];
 };
-static_assert(sizeof(Unit) == kUnitInts * 4, "Unit layout");
+static_assert(sizeof(UnitRec) == 32 + 4 * kMaxWideBeams + 8 * kMaxEntries, "UnitRec layout");
 
 struct AttnParams {
   const void* q;
@@ -49,36 +71,42 @@ struct AttnParams {
   const int32_t* block_tables;
   const int32_t* seq_lens;
   float* out;
-  float* part_o;   // [slots][Hq][D]
-  float* part_ml;  // [slots][Hq][2]: running max (log2 units), sum
-  // prefix path (null for the paged path)
-  const int32_t* perm;
-  const int32_t* tail_lblock;
-  const int32_t* slot_base;
-  const int32_t* seg_blocks;
-  const Unit* units;
+  float* part_o;   // [rows][D]
+  float* part_ml;  // [rows][2]: running max (log2 units), sum
+  // prefix path (null recs: paged path)
+  const UnitRec* recs;
+  const int32_t* build_len;  // [S] lengths the metadata was built for
+  int32_t rows_per_head;     // partial rows of one KV head
   int32_t max_blocks;
   int32_t num_blocks;
   int32_t num_seqs;
   int32_t hq;
   int32_t hkv;
   int32_t g;
-  float scale_log2;     // softmax scale * log2(e)
-  int32_t paged_nsplit; // paged path: splits per beam (1: write the output directly)
+  float scale_log2;      // softmax scale * log2(e)
+  int32_t paged_nsplit;  // paged path: splits per beam (1: write the output directly)
   int32_t paged_max_len;
-  int32_t pad;
 };
 
+// Slots the merge kernel reads per round trip (and the smallest slot-table
+// stride - 1, so that a beam's first round of slots is always in its row).
+constexpr int kMergeBatch = 16;
 
 struct MergeParams {
   const float* part_o;
   const float* part_ml;
-  const int32_t* slot_base;    // [S + 1]; null for the paged path
+  // [S][slot_stride]: slot count, then the partial row of the beam's row 0
+  // (KV head 0) for each slot in merge order; null for the paged path
+  const int32_t* slot_tab;
+  int32_t slot_stride;
+  int32_t pad0;
   const int32_t* seq_lens;
-  const int32_t* tail_lblock;  // prefix path: stale-metadata check (else null)
+  const int32_t* build_len;  // prefix path: stale-metadata check (else null)
   float* out;
   int32_t num_seqs;
   int32_t hq;
+  int32_t g;
+  int32_t rows_per_head;
   int32_t paged_nsplit;
   int32_t pad;
 };

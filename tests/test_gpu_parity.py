@@ -104,15 +104,19 @@ def _duplicate_beams(wl, picks):
         req_seq_offsets=offs)
 
 
-def test_identical_beams_bit_identical():
+def test_identical_beams_agree():
+    """Beams with identical tables, lengths and queries get the same rows. The paged path computes
+    them with the same instruction sequence (bit-identical); the prefix path may place the two
+    beams' private blocks in different lanes of a block pair or on different waves, so their fp32
+    sums associate differently (agreement to fp32 rounding, far inside the parity tolerance)."""
     wl = make_workload("1p5b16", 0)
     picks = [0, 5, 9]
     wl2 = _duplicate_beams(wl, picks)
     op, ox = outputs(wl2)
     s = wl.num_seqs
     for i, b in enumerate(picks):
-        assert np.array_equal(ox[b], ox[s + i])
         assert np.array_equal(op[b], op[s + i])
+        assert err(ox[b], ox[s + i]) <= 1e-5
     ref = oracle_attn_workload(wl2)
     assert err(ox, ref) <= TOL["bf16"]
 
@@ -194,13 +198,20 @@ def test_private_appends_after_build():
 
 
 def test_bad_block_id_gives_nan_row_only():
+    """A block id outside the pool makes only that beam's row NaN: in the paged path for any table
+    entry, in the prefix path for a block appended after the metadata was built (entries in use at
+    build time are validated by tts_build_prefix_meta)."""
     wl = make_workload("1p5b16", 0)
-    x, paged, pref = runners(wl)
-    good_p, good_x = paged().clone(), pref().clone()
     m = oracle_prefix_meta(wl.req_seq_offsets, wl.block_tables, wl.seq_lens, 16)
     b = 3
     last = (int(wl.seq_lens[b]) + 15) // 16 - 1
-    assert last >= m["tail_lblock"][b]  # a tail block
+    assert last > m["tail_lblock"][b]  # a tail block that is not the first one
+    short = wl.seq_lens.copy()
+    short[b] = 16 * last  # metadata built before block `last` was appended
+    x, paged, pref = runners(wl, lens_for_meta=short)
+    good_p, good_x = paged().clone(), pref().clone()
+    ref = oracle_attn_workload(wl)
+    assert err(good_x.cpu().numpy(), ref) <= TOL["bf16"]
     x.block_tables[b, last] = wl.num_blocks + 1000
     op, ox = paged(), pref()
     torch.cuda.synchronize()
@@ -241,6 +252,7 @@ def test_work_plan_stats_and_workspace():
     x, paged, pref = runners(wl)
     units, slots = pref.meta.stats()
     assert units > 0 and slots >= wl.num_seqs
+    # every merge slot of a beam is one partial row per query head
     assert pref.ws_bytes >= slots * wl.shape.num_q_heads * (wl.shape.head_dim + 2) * 4
 
 
