@@ -116,7 +116,7 @@ def cpu_baseline(wl, budget_s):
 
 
 COPY_KERNEL = "bitwise_not"  # the calibration copy: dst = ~src, one read and one write per byte
-ATTN_KERNEL = "attn_units_kernel"
+ATTN_KERNEL = "attn_kernel"
 
 
 def _counter_rows(path, counter):
@@ -313,8 +313,8 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "attn_units_kernel (work units of tts_prefix_decode_partials)" if args.variant == "prefix"
-                      else "attn_units_kernel + merge_kernel (tts_paged_decode_attn)",
+            "kernel": "attn_kernel (work units of tts_prefix_decode_partials)" if args.variant == "prefix"
+                      else "attn_kernel + merge_kernel (tts_paged_decode_attn)",
             "achieved": achieved,
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
