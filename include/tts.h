@@ -208,8 +208,10 @@ tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta*
 /* The two launches of tts_prefix_decode_attn, for callers that schedule
  * them separately (to overlap the merge with other work, or to time the
  * attention kernel alone). tts_prefix_decode_partials runs the work units
- * and leaves one partial softmax state (running max, sum, unnormalised
- * output row) per (beam, query head, slot) in the workspace;
+ * and leaves one partial softmax state (reference max, sum, and the output
+ * row normalised by that sum, in fp16 with a power-of-two row scale for
+ * bf16 and fp8 caches, in fp32 for fp32 caches) per (beam, query head,
+ * slot) in the workspace;
  * tts_prefix_decode_merge combines each beam's states, in slot order, into
  * out. Arguments and rules are those of tts_prefix_decode_attn; the merge
  * must follow the partials call on the same workspace in stream order, with

@@ -16,7 +16,7 @@
 
 namespace tts {
 hipError_t launch_attn(const AttnParams& p, int grid, int head_dim, int kv_kind, hipStream_t stream);
-hipError_t launch_merge(const MergeParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_merge(const MergeParams& p, int head_dim, int kv_kind, hipStream_t stream);
 }  // namespace tts
 
 namespace {
@@ -70,6 +70,11 @@ tts_status check_scales(const tts_attn_desc* d, const float* ks, const float* vs
 }
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+// Partial-state elements: fp16 for bf16 and fp8 caches, fp32 for fp32 caches.
+size_t part_o_bytes(const tts_attn_desc* d, size_t rows) {
+  return align256(rows * d->head_dim * (d->kv_dtype == TTS_F32 ? 4 : 2));
+}
 
 }  // namespace
 
@@ -227,7 +232,7 @@ size_t tts_paged_decode_workspace_size(const tts_attn_desc* d, int32_t num_seqs,
   const int32_t ns = paged_nsplit(max_seq_len);
   if (ns == 1) return 0;
   const size_t rows = static_cast<size_t>(num_seqs) * ns * d->num_q_heads;
-  return align256(rows * d->head_dim * 4) + align256(rows * 2 * 4);
+  return part_o_bytes(d, rows) + align256(rows * tts::kPartMl * 4);
 }
 
 tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const void* q, const void* k_cache,
@@ -259,8 +264,8 @@ tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const
   p.block_tables = block_tables;
   p.seq_lens = seq_lens;
   p.out = static_cast<float*>(out);
-  p.part_o = ns > 1 ? static_cast<float*>(workspace) : nullptr;
-  p.part_ml = ns > 1 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * d->head_dim * 4))
+  p.part_o = ns > 1 ? workspace : nullptr;
+  p.part_ml = ns > 1 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + part_o_bytes(d, rows))
                      : nullptr;
 
   p.max_blocks = max_blocks_per_seq;
@@ -286,7 +291,7 @@ tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const
     mp.hq = d->num_q_heads;
     mp.g = d->num_q_heads / d->num_kv_heads;
     mp.paged_nsplit = ns;
-    e = tts::launch_merge(mp, d->head_dim, stream);
+    e = tts::launch_merge(mp, d->head_dim, kv_kind(d), stream);
     if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
   }
   return ok();
@@ -295,7 +300,7 @@ tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const
 size_t tts_prefix_decode_workspace_size(const tts_attn_desc* d, const tts_prefix_meta* m) {
   if (!d || !m || !m->has_plan || check_desc(d) != TTS_OK) return 0;
   const size_t rows = static_cast<size_t>(m->plan.rows_per_head) * d->num_kv_heads;
-  return align256(rows * d->head_dim * 4) + align256(rows * 2 * 4);
+  return part_o_bytes(d, rows) + align256(rows * tts::kPartMl * 4);
 }
 
 namespace {
@@ -338,8 +343,8 @@ tts_status prefix_params(const tts_attn_desc* d, const tts_prefix_meta* m, const
   p->block_tables = block_tables;
   p->seq_lens = seq_lens;
   p->out = static_cast<float*>(out);
-  p->part_o = static_cast<float*>(workspace);
-  p->part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) + align256(rows * d->head_dim * 4));
+  p->part_o = workspace;
+  p->part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) + part_o_bytes(d, rows));
   p->recs = reinterpret_cast<const tts::UnitRec*>(dev + m->off_recs);
   p->build_len = reinterpret_cast<const int32_t*>(dev + m->off_build);
   p->rows_per_head = m->plan.rows_per_head;
@@ -375,7 +380,7 @@ tts_status launch_prefix_merge(const tts_attn_desc* d, const tts_prefix_meta* m,
   mp.hq = d->num_q_heads;
   mp.g = p.g;
   mp.rows_per_head = p.rows_per_head;
-  hipError_t e = tts::launch_merge(mp, d->head_dim, stream);
+  hipError_t e = tts::launch_merge(mp, d->head_dim, kv_kind(d), stream);
   if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
   return TTS_OK;
 }

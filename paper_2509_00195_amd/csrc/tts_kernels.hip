@@ -115,6 +115,54 @@ __device__ __forceinline__ float xlane_sum16(float x) {
   return x + __shfl_xor(x, 32);
 }
 
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+// Writes a row's partial state: m, l and o / (l s) in the partial layout
+// (fp16 elements with a power-of-two row scale s for bf16 and fp8 caches,
+// fp32 with s = 1 for fp32 caches; elements in lane order). Lane (ln, lq)
+// holds dimensions 16 t + 4 lq + j of row ln in o[t][j]; the four lanes of
+// a row call together (the scale is reduced across them), `active` says
+// whether the row exists.
+template <int D, int KV>
+__device__ __forceinline__ void write_partial(void* part_o, float* part_ml, int64_t prow, const f32x4 (&o)[D / 16],
+                                              float m, float l, int lq, bool active) {
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  int e = 0;
+  if constexpr (KV != kKvF32) {
+    float amax = 0.f;
+#pragma unroll
+    for (int t = 0; t < D / 16; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) amax = fmaxf(amax, __builtin_fabsf(o[t][j]));
+    amax *= inv;
+    amax = fmaxf(amax, __shfl_xor(amax, 16));
+    amax = fmaxf(amax, __shfl_xor(amax, 32));
+    // amax = f 2^e with f in [0.5, 1): every element over 2^e is in [-1, 1].
+    if (amax > 0.f && amax <= 3.0e38f) e = __builtin_amdgcn_frexp_expf(amax);
+  }
+  if (!active) return;
+  if constexpr (KV != kKvF32) {
+    uint32_t w[D / 8];
+#pragma unroll
+    for (int t = 0; t < D / 16; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; j += 2) {
+        const f16x2 h = {static_cast<_Float16>(__builtin_ldexpf(o[t][j] * inv, -e)),
+                         static_cast<_Float16>(__builtin_ldexpf(o[t][j + 1] * inv, -e))};
+        w[2 * t + j / 2] = __builtin_bit_cast(uint32_t, h);
+      }
+    uint4* dst = reinterpret_cast<uint4*>(static_cast<uint16_t*>(part_o) + prow * D + (D / 4) * lq);
+#pragma unroll
+    for (int c = 0; c < D / 32; ++c) dst[c] = uint4{w[4 * c], w[4 * c + 1], w[4 * c + 2], w[4 * c + 3]};
+  } else {
+    f32x4* dst = reinterpret_cast<f32x4*>(static_cast<float*>(part_o) + prow * D + (D / 4) * lq);
+#pragma unroll
+    for (int t = 0; t < D / 16; ++t) dst[t] = o[t] * inv;
+  }
+  if (lq == 0)
+    *reinterpret_cast<f32x4*>(part_ml + prow * kPartMl) = f32x4{m, l, __builtin_ldexpf(1.f, e), 0.f};
+}
+
 __device__ __forceinline__ int rl(int x, int i) { return __builtin_amdgcn_readlane(x, i); }
 __device__ __forceinline__ float rlf(float x, int i) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), i));
@@ -805,15 +853,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
         // Each wave writes the partial states of its own rows.
 #pragma unroll
         for (int i = 0; i < kWideTiles; ++i) {
+          if (wave + kWaves * i >= nt) continue;  // wave-uniform
           const int row = 16 * (wave + kWaves * i) + ln;
           const float l = xlane_sum16(st[i].l);
-          if (row < nrows) {
-            const int64_t prow = static_cast<int64_t>(kvh) * p.rows_per_head + prow0 + row;
-            float* po = p.part_o + prow * D;
-#pragma unroll
-            for (int d = 0; d < D / 16; ++d) *reinterpret_cast<f32x4*>(po + 16 * d + 4 * lq) = st[i].o[d];
-            if (lq == 0) *reinterpret_cast<f32x2*>(p.part_ml + prow * 2) = f32x2{st[i].m, l};
-          }
+          const int64_t prow = static_cast<int64_t>(kvh) * p.rows_per_head + prow0 + row;
+          write_partial<D, KV>(p.part_o, p.part_ml, prow, st[i].o, st[i].m, l, lq, row < nrows);
         }
         TTS_PROF_MARK(2, rec_idx);
         const int nu_rows_w = rfl(nu.nrows);
@@ -1056,10 +1100,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             prow = (static_cast<int64_t>(paged_b) * p.paged_nsplit + paged_split) * p.hq + kvh * p.g + row;
           else
             prow = static_cast<int64_t>(kvh) * p.rows_per_head + prow0 + row;
-          float* po = p.part_o + prow * D;
-#pragma unroll
-          for (int dt = 0; dt < D / 16; ++dt) *reinterpret_cast<f32x4*>(po + 16 * dt + 4 * lq) = o[dt];
-          if (lq == 0) *reinterpret_cast<f32x2*>(p.part_ml + prow * 2) = f32x2{m_fin, l};
+          write_partial<D, KV>(p.part_o, p.part_ml, prow, o, m_fin, l, lq, true);
         }
       }
     }
@@ -1077,20 +1118,23 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
 }
 
 // Exact merge of the partial softmax states of each (beam, query head), in
-// the order of the beam's slot list:
-//   m = max_k m_k,  l = sum_k l_k 2^(m_k - m),  out = sum_k o_k 2^(m_k - m) / l.
+// the order of the beam's slot list. With M = max_k m_k and
+// w_k = l_k 2^(m_k - M), and e_k the stored elements o_k / (l_k s_k):
+//   out = sum_k w_k s_k e_k / sum_k w_k.
 // One wave per row (2 output dims per lane). A row's slot count and first
 // kMergeBatch slots sit in one row of the slot table and are loaded together
 // with the beam's lengths; then the states of kMergeBatch slots at a time,
 // so a row costs two round trips to memory (more only past kMergeBatch
 // slots).
-template <int D>
+template <int D, bool F16>
 __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
   constexpr int kTpr = D / 2;
   constexpr int kRows = kThreads / kTpr;
   constexpr int kBatch = kMergeBatch;
   const int r = blockIdx.x * kRows + threadIdx.x / kTpr;
-  const int d0 = (threadIdx.x % kTpr) * 2;
+  // Stored position pos0 (lane order) holds dimension d0, pos0 + 1 holds d0 + 1.
+  const int pos0 = (threadIdx.x % kTpr) * 2;
+  const int d0 = 16 * ((pos0 % (D / 4)) / 4) + 4 * (pos0 / (D / 4)) + pos0 % 4;
   if (r >= p.num_seqs * p.hq) return;
   const int b = r / p.hq;
   const int h = r % p.hq;
@@ -1111,14 +1155,15 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
   }
   const int L = p.seq_lens[b];
   bool nan = p.build_len && L < p.build_len[b];
-  float mx = kNegInf, l = 0.f;
+  float mx = kNegInf, den = 0.f;
   f32x2 acc = {0.f, 0.f};
   for (int k0 = 0; k0 < n; k0 += kBatch) {
     if (k0 > 0 && tab) {
 #pragma unroll
       for (int k = 0; k < kBatch; ++k) ent[k] = k0 + k < n ? tab[1 + k0 + k] : 0;
     }
-    f32x2 ml[kBatch], o[kBatch];
+    f32x4 ml[kBatch];
+    f32x2 o[kBatch];
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
       const int kk = k0 + k < n ? k0 + k : n - 1;
@@ -1127,12 +1172,17 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
         row = head_base + (k0 + k < n ? ent[k] : ent[0]);
       else
         row = (static_cast<int64_t>(b) * p.paged_nsplit + kk) * p.hq + h;
-      ml[k] = *reinterpret_cast<const f32x2*>(p.part_ml + row * 2);
-      o[k] = *reinterpret_cast<const f32x2*>(p.part_o + row * D + d0);
+      ml[k] = *reinterpret_cast<const f32x4*>(p.part_ml + row * kPartMl);
+      if constexpr (F16) {
+        const f16x2 hv = *reinterpret_cast<const f16x2*>(static_cast<const uint16_t*>(p.part_o) + row * D + pos0);
+        o[k] = f32x2{static_cast<float>(hv.x), static_cast<float>(hv.y)};
+      } else {
+        o[k] = *reinterpret_cast<const f32x2*>(static_cast<const float*>(p.part_o) + row * D + pos0);
+      }
     }
 #pragma unroll
     for (int k = 0; k < kBatch; ++k)
-      if (k0 + k >= n) ml[k] = f32x2{kNegInf, 0.f};
+      if (k0 + k >= n) ml[k] = f32x4{kNegInf, 0.f, 0.f, 0.f};
     float bm = kNegInf;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
@@ -1142,17 +1192,17 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
     const float mn = fmaxf(mx, bm);
     if (mn == kNegInf) continue;
     const float a = (mx == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(mx - mn);
-    l *= a;
+    den *= a;
     acc *= a;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
-      const float fct = (ml[k].x == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(ml[k].x - mn);
-      l += ml[k].y * fct;
-      acc += o[k] * fct;
+      const float w = (ml[k].x == kNegInf) ? 0.f : ml[k].y * __builtin_amdgcn_exp2f(ml[k].x - mn);
+      den += w;
+      acc += o[k] * (w * ml[k].z);
     }
     mx = mn;
   }
-  const float inv = (l > 0.f && L > 0) ? 1.f / l : 0.f;
+  const float inv = (den > 0.f && L > 0) ? 1.f / den : 0.f;
   f32x2 w = acc * inv;
   if (nan) {
     const float q = __builtin_nanf("");
@@ -1167,15 +1217,23 @@ static hipError_t launch_attn_t(const AttnParams& p, int grid, hipStream_t strea
   return hipGetLastError();
 }
 
-hipError_t launch_merge(const MergeParams& p, int head_dim, hipStream_t stream) {
+hipError_t launch_merge(const MergeParams& p, int head_dim, int kv_kind, hipStream_t stream) {
   const int rows = p.num_seqs * p.hq;
   if (rows <= 0) return hipSuccess;
   const int per = kThreads / (head_dim / 2);
   const int blocks = (rows + per - 1) / per;
-  if (head_dim == 128)
-    hipLaunchKernelGGL((merge_kernel<128>), dim3(blocks), dim3(kThreads), 0, stream, p);
-  else
-    hipLaunchKernelGGL((merge_kernel<64>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  const bool f16 = kv_kind != kKvF32;
+  if (head_dim == 128) {
+    if (f16)
+      hipLaunchKernelGGL((merge_kernel<128, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+    else
+      hipLaunchKernelGGL((merge_kernel<128, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  } else {
+    if (f16)
+      hipLaunchKernelGGL((merge_kernel<64, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+    else
+      hipLaunchKernelGGL((merge_kernel<64, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+  }
   return hipGetLastError();
 }
 

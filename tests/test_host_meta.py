@@ -148,4 +148,6 @@ def test_paged_workspace_size():
     ws = tts.tts_paged_decode_workspace_size(d, 64, 4096)
     nsplit = -(-256 // 32)
     rows = 64 * nsplit * 28
-    assert ws >= rows * 130 * 4
+    assert ws >= rows * (128 * 2 + 16)  # fp16 row + max, sum, scale, pad
+    d32 = tts.make_desc(28, 4, 128, q_dtype="f32", kv_dtype="f32")
+    assert tts.tts_paged_decode_workspace_size(d32, 64, 4096) >= rows * (128 * 4 + 16)
