@@ -285,7 +285,7 @@ struct RowState {
   f32x4 o[D / 16];
   float m;     // reference (log2 units), uniform over the 4 lanes of a row
   float l;     // per-lane partial sum
-  float seen;  // largest scaled score this lane has seen (-inf: none)
+  float seen;  // largest exponent argument (scaled score - m) this lane has seen (-inf: none)
 };
 
 // Uniform description of one pair: blocks' valid tokens, row ranges and
@@ -344,14 +344,15 @@ __device__ __forceinline__ void tile_step(const Ops<D, KV>& f, const QFrag<D, KV
   // block lq >> 1, at slots 8(lq & 1) + 4t + i.
   const bool hi = lq >= 2;
   const float sc = hi ? pi.ks1 : pi.ks0;
-  // fp8 block scales are caller data (any sign): scale first there. For the
-  // others the positive scale preserves the maximum and goes into exp2.
-  constexpr bool kPreScale = KV == kKvFp8;
-  float s[8];
+  // Exponent arguments x = score * scale - m (the fp8 K scale is part of
+  // `sc`), masked to -inf past the valid tokens and outside the rows the
+  // blocks apply to. `seen` tracks the largest x: it is taken over the fma
+  // results, which are canonical, so the maximum needs no NaN quieting.
+  float x[8];
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) s[4 * t + i] = kPreScale ? acc[t][i] * sc : acc[t][i];
+    for (int i = 0; i < 4; ++i) x[4 * t + i] = __builtin_fmaf(acc[t][i], sc, -st.m);
   const int row = 16 * r + ln;
   const int valid = hi ? pi.v1 : pi.v0;
   const int ra = hi ? pi.a1 : pi.a0, re = hi ? pi.e1 : pi.e0;
@@ -361,17 +362,14 @@ __device__ __forceinline__ void tile_step(const Ops<D, KV>& f, const QFrag<D, KV
     const int lim = (row >= ra && row < re) ? valid : 0;
     const int slot0 = 8 * (lq & 1);
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (slot0 + 4 * t + i >= lim) s[4 * t + i] = kNegInf;
+    for (int i = 0; i < 8; ++i)
+      if (slot0 + i >= lim) x[i] = kNegInf;
   }
-  float smax = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
-  st.seen = fmaxf(st.seen, kPreScale ? smax : smax * sc);
+  st.seen = fmaxf(fmaxf(fmaxf(fmaxf(st.seen, x[0]), fmaxf(x[1], x[2])), fmaxf(x[3], x[4])),
+                  fmaxf(fmaxf(x[5], x[6]), x[7]));
   float p[8];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
-    p[i] = __builtin_amdgcn_exp2f(kPreScale ? s[i] - st.m : __builtin_fmaf(s[i], sc, -st.m));
+  for (int i = 0; i < 8; ++i) p[i] = __builtin_amdgcn_exp2f(x[i]);
   st.l += ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
   if constexpr (O::f32) {
 #pragma unroll
