@@ -65,6 +65,7 @@ constexpr int kWaves = 4;
 constexpr int kTiles = kMaxRows / 16;
 constexpr int kWideTiles = kMaxWideRows / 16 / 4;  // row tiles per wave in a wide unit
 constexpr float kNegInf = -__builtin_inff();
+constexpr float kInf = __builtin_inff();
 constexpr float kRefWindow = 64.0f;  // |row max| (log2 units) handled with m_ref = 0
 
 enum KvKind : int { kKvF32 = 0, kKvBf16 = 1, kKvFp8 = 2 };
@@ -316,7 +317,11 @@ __device__ __forceinline__ QFrag<D, KV> q_from_lds(const unsigned char* qlds, in
   return qf;
 }
 
-template <int D, int KV>
+// kWide: the pair applies to every row of the tile (rows past the unit's
+// end hold zero queries and are never written) and only a missing second
+// block (pi.v1 == 0) is masked, by a reference of +inf for its half of the
+// lanes: no branch, so the compiler interleaves consecutive tiles.
+template <int D, int KV, bool kWide = false>
 __device__ __forceinline__ void tile_step(const Ops<D, KV>& f, const QFrag<D, KV>& qfr, RowState<D>& st,
                                           const PairInfo& pi, int r, int ln, int lq) {
   using O = Ops<D, KV>;
@@ -349,16 +354,17 @@ __device__ __forceinline__ void tile_step(const Ops<D, KV>& f, const QFrag<D, KV
   // blocks apply to. `seen` tracks the largest x: it is taken over the fma
   // results, which are canonical, so the maximum needs no NaN quieting.
   float x[8];
+  const float mref = (kWide && hi && pi.v1 == 0) ? kInf : st.m;
 #pragma unroll
   for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) x[4 * t + i] = __builtin_fmaf(acc[t][i], sc, -st.m);
+    for (int i = 0; i < 4; ++i) x[4 * t + i] = __builtin_fmaf(acc[t][i], sc, -mref);
   const int row = 16 * r + ln;
   const int valid = hi ? pi.v1 : pi.v0;
   const int ra = hi ? pi.a1 : pi.a0, re = hi ? pi.e1 : pi.e0;
   const bool full = pi.v0 == kTok && pi.v1 == kTok && pi.a0 <= 16 * r && pi.e0 >= 16 * r + 16 &&
                     pi.a1 <= 16 * r && pi.e1 >= 16 * r + 16;
-  if (!full) {
+  if (!kWide && !full) {
     const int lim = (row >= ra && row < re) ? valid : 0;
     const int slot0 = 8 * (lq & 1);
 #pragma unroll
@@ -685,7 +691,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
   // Wide units (bf16) use the area after the query rows for their pair
   // stages instead.
   constexpr int kCombBytes = kWaves * (kTiles - 1) * G::comb_floats * 4;
-  constexpr int kStageBytes = KV == kKvBf16 ? 2 * Stage<D, KV>::bytes : 0;
+  // Wide units: two pair stages and the waves' query fragments.
+  constexpr int kWideQBytes = kWaves * kWideTiles * Ops<D, KV>::kk * 64 * 16;
+  constexpr int kStageBytes = KV == kKvBf16 ? 2 * Stage<D, KV>::bytes + kWideQBytes : 0;
   constexpr int kAreaBytes = kCombBytes > kStageBytes ? kCombBytes : kStageBytes;
   __shared__ __attribute__((aligned(16))) unsigned char lds[Q::bytes + kAreaBytes];
   unsigned char* qbuf = lds;
@@ -788,7 +796,12 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             qw[i].q[j] = ok ? *reinterpret_cast<const uint4*>(qrow + 32 * j + 8 * lq) : uint4{0u, 0u, 0u, 0u};
         }
         unsigned char* stages = lds + Q::bytes;
+        // This wave's query fragments, [tile][k step][lane] x 16 bytes: read
+        // back per tile and pair (registers are the scarcer resource here).
+        unsigned char* wq = stages + 2 * SG::bytes + wave * (kWideQBytes / kWaves);
+        auto wq_at = [&](int i, int j) { return wq + ((i * Ops<D, KV>::kk + j) * 64 + lane) * 16; };
         const int np = (nst + 1) >> 1;
+        const int tpw = (nt + kWaves - 1) / kWaves;
         auto pair_ids = [&](int pp, int* id0, int* id1) {
           pp = pp < np ? pp : np - 1;  // past the end: a repeat of the last pair (a cache hit, never used)
           *id0 = rl(u.ent_id, 2 * pp);
@@ -828,9 +841,17 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             pi.ks0 = pi.ks1 = sc_w;
             pi.vs0 = pi.vs1 = 1.f;
             if (pi.v1 == 0) mask_v<D, KV>(o, lq, pi.v0, pi.v1);
+            // The unit's tiles per wave (uniform): one straight-line block
+            // per count, so the compiler interleaves the tiles' products.
+            if (tpw >= kWideTiles) {
 #pragma unroll
-            for (int i = 0; i < kWideTiles; ++i)
-              if (wave + kWaves * i < nt) tile_step<D, KV>(o, qw[i], st[i], pi, wave + kWaves * i, ln, lq);
+              for (int i = 0; i < kWideTiles; ++i) tile_step<D, KV, true>(o, qw[i], st[i], pi, wave + kWaves * i, ln, lq);
+            } else if (tpw == 2) {
+#pragma unroll
+              for (int i = 0; i < 2; ++i) tile_step<D, KV, true>(o, qw[i], st[i], pi, wave + kWaves * i, ln, lq);
+            } else {
+              tile_step<D, KV, true>(o, qw[0], st[0], pi, wave, ln, lq);
+            }
           };
           for (int pp = 0; pp < np; pp += 2) {
             step(qa, qb, pp);
