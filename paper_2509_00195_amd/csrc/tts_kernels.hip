@@ -691,9 +691,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
   // Wide units (bf16) use the area after the query rows for their pair
   // stages instead.
   constexpr int kCombBytes = kWaves * (kTiles - 1) * G::comb_floats * 4;
-  // Wide units: two pair stages and the waves' query fragments.
-  constexpr int kWideQBytes = kWaves * kWideTiles * Ops<D, KV>::kk * 64 * 16;
-  constexpr int kStageBytes = KV == kKvBf16 ? 2 * Stage<D, KV>::bytes + kWideQBytes : 0;
+  constexpr int kStageBytes = KV == kKvBf16 ? 2 * Stage<D, KV>::bytes : 0;
   constexpr int kAreaBytes = kCombBytes > kStageBytes ? kCombBytes : kStageBytes;
   __shared__ __attribute__((aligned(16))) unsigned char lds[Q::bytes + kAreaBytes];
   unsigned char* qbuf = lds;
@@ -796,10 +794,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             qw[i].q[j] = ok ? *reinterpret_cast<const uint4*>(qrow + 32 * j + 8 * lq) : uint4{0u, 0u, 0u, 0u};
         }
         unsigned char* stages = lds + Q::bytes;
-        // This wave's query fragments, [tile][k step][lane] x 16 bytes: read
-        // back per tile and pair (registers are the scarcer resource here).
-        unsigned char* wq = stages + 2 * SG::bytes + wave * (kWideQBytes / kWaves);
-        auto wq_at = [&](int i, int j) { return wq + ((i * Ops<D, KV>::kk + j) * 64 + lane) * 16; };
         const int np = (nst + 1) >> 1;
         const int tpw = (nt + kWaves - 1) / kWaves;
         auto pair_ids = [&](int pp, int* id0, int* id1) {
