@@ -270,6 +270,15 @@ def main():
         kms = ms_per_step
     kv_bytes = unique_kv if args.variant == "prefix" else logical_kv
     achieved = kv_bytes / (kms * 1e-3) / 1e9
+
+    # Streaming calibration on the same GPU: an elementwise copy of 1 GiB
+    # (dst = ~src), one read and one write per byte, timed the same way.
+    csrc = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+    cdst = torch.empty_like(csrc)
+    torch.bitwise_not(csrc, out=cdst)
+    cms = timed(lambda n: [torch.bitwise_not(csrc, out=cdst) for _ in range(n)], 20) / 20
+    stream_gbs = 2.0 * csrc.numel() / (cms * 1e-3) / 1e9
+    del csrc, cdst
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
         with open(TRAFFIC_FILE) as f:
@@ -303,6 +312,8 @@ def main():
             "logical_kv_bytes": int(logical_kv),
             "sharing": logical_kv / max(unique_kv, 1),
             "unique_kv_hbm_frac_per_call": unique_kv / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
+            "stream_copy_gbs": stream_gbs,
+            "attention_frac_of_stream_copy": achieved / stream_gbs,
             "attention_kernel_us": kms * 1e3,
             "merge_and_gaps_us": (ms_per_step - kms) * 1e3,
             "per_28_layer_step_beam_tokens_per_s": value / 28.0,

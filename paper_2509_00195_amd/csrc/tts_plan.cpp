@@ -33,39 +33,38 @@
 namespace tts {
 namespace {
 
-// Cost model (microseconds of one workgroup). A unit streams its KV blocks,
-// its query rows and its partial states (written here, read again by the
-// merge) through the compute unit's share of memory bandwidth, and runs
-// the matrix work of its row tiles x block pairs on four SIMDs; the two
-// overlap, plus a fixed part (record, barriers, combine).
-constexpr double kBytesPerUs = 5.0e6 / 256;  // ~5 TB/s over 256 compute units
-constexpr double kTilePairUs = 350.0 / 2400.0;  // one 16-row tile x one block pair, 2.4 GHz
-constexpr double kUnitFixedUs = 0.8;
-#ifndef TTS_UNITS_PER_BIN
-#define TTS_UNITS_PER_BIN 0.5
-#endif
-constexpr double kUnitsPerBin = TTS_UNITS_PER_BIN;
-constexpr double kMinUnitUs = 3.0;
+// Cost model (microseconds of one workgroup, all compute units busy),
+// fitted to per-unit clock marks of the kernel at the 7B-shaped 64-beam
+// tree (D 128, bf16 KV, g 7): every unit pays a fixed part (its first
+// memory round trips, the end of its loop, the partial writes); a narrow
+// unit then streams its blocks at about 0.166 us per 8 KiB block and pays
+// about 0.064 us per query row (query read, combine, partial state); a wide
+// unit pays about 0.193 us per 8 KiB block for staging it through LDS plus
+// 0.113 us per block for each row tile a wave runs. Other shapes scale the
+// block terms by their bytes and the tile term by the head size.
+constexpr double kUnitFixedUs = 4.9;
+constexpr double kNarrowUsPerByte = 0.166 / 8192;
+constexpr double kRowUs = 0.064;  // per row of 256 + 272 bytes (query + partial state)
+constexpr double kWideUsPerByte = 0.193 / 8192;
+constexpr double kTileBlockUs = 0.113;  // per block and row tile of a wave, D = 128
 constexpr int kXcds = 8;  // workgroup k of a launch runs on XCD k % 8
 
 int tiles_of(int rows) { return (rows + 15) / 16; }
 
 struct CostModel {
-  double blk_bytes, q_row_bytes, part_row_bytes;
-  double mem_us(double blocks, int rows) const {
-    return (blocks * blk_bytes + rows * (q_row_bytes + part_row_bytes)) / kBytesPerUs;
-  }
+  double blk_bytes, q_row_bytes, part_row_bytes, d_scale;
+  double row_us() const { return kRowUs * (q_row_bytes + part_row_bytes) / 528.0; }
   // Narrow units: the waves split the block pairs, every wave runs every tile.
   double narrow_us(int blocks, int rows) const {
-    const double comp = tiles_of(rows) * ((blocks + 1) / 2) * kTilePairUs / 4.0;
-    return std::max(mem_us(blocks, rows), comp) + kUnitFixedUs;
+    return kUnitFixedUs + blocks * blk_bytes * kNarrowUsPerByte + rows * row_us();
   }
   // Wide units: every wave runs every pair on its quarter of the tiles.
   double wide_us(int blocks, int rows) const {
-    const double comp = ((tiles_of(rows) + 3) / 4) * ((blocks + 1) / 2) * kTilePairUs;
-    return std::max(mem_us(blocks, rows), comp) + kUnitFixedUs;
+    const int tpw = (tiles_of(rows) + 3) / 4;
+    return kUnitFixedUs + blocks * (blk_bytes * kWideUsPerByte + tpw * kTileBlockUs * d_scale);
   }
-  double bytes(int blocks, int rows) const { return mem_us(blocks, rows) * kBytesPerUs; }
+  // Bytes a unit moves: its blocks, its query rows, its partial states.
+  double bytes(int blocks, int rows) const { return blocks * blk_bytes + rows * (q_row_bytes + part_row_bytes); }
 };
 
 struct Tmpl {
@@ -83,6 +82,10 @@ struct NItem {
   int32_t p0, p1;
   int32_t valid;
   uint32_t flags;
+};
+
+struct Work {
+  int32_t t, kvh;
   double cost;
 };
 
@@ -107,8 +110,9 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
   CostModel cm;
   cm.blk_bytes = 2.0 * bs * shape.head_dim * shape.kv_bytes;
   cm.q_row_bytes = shape.head_dim * (shape.kv_bytes == 4 ? 4.0 : 2.0);
-  cm.part_row_bytes = 2.0 * (shape.head_dim + 2) * 4.0;
-  const double blk_us = cm.blk_bytes / kBytesPerUs;
+  // A partial state is written once and read once by the merge.
+  cm.part_row_bytes = 2.0 * (shape.head_dim * (shape.kv_bytes == 4 ? 4.0 : 2.0) + 4 * kPartMl);
+  cm.d_scale = shape.head_dim / 128.0;
 
   // ---- tree structure ----------------------------------------------------
   std::vector<std::vector<int32_t>> children(nseg), leaves(nseg);
@@ -146,9 +150,9 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
     for (int32_t j = m.tail_lblock[b]; j < nb; ++j) {
       const int32_t v = std::min(bs, L - j * bs);
       const uint32_t fl = (j == nb - 1 && v < bs) ? kEntLive : 0u;
-      items.push_back({m.tables[static_cast<size_t>(b) * m.max_blocks + j], pos, pos + 1, v, fl, blk_us});
+      items.push_back({m.tables[static_cast<size_t>(b) * m.max_blocks + j], pos, pos + 1, v, fl});
     }
-    items.push_back({0, pos, pos + 1, 1, kEntExt, 0.0});
+    items.push_back({0, pos, pos + 1, 1, kEntExt});
   };
   // Iterative walk: a stack of (segment, or -1 - leaf position).
   std::vector<int32_t> stack;
@@ -169,7 +173,7 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
       const int32_t bb = m.seg_beam_begin[x], be = m.seg_beam_end[x];
       if (!wide[x]) {
         for (int32_t j = 0; j < m.seg_nblocks[x]; ++j)
-          items.push_back({seg_block(x, j), bb, be, bs, 0u, blk_us});
+          items.push_back({seg_block(x, j), bb, be, bs, 0u});
       }
       tmp.clear();
       for (int32_t c : children[x]) tmp.push_back({m.seg_beam_begin[c], c});
@@ -178,83 +182,77 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
     }
   }
 
-  // ---- target unit time ---------------------------------------------------
-  // Lower bound of the work per KV head: every block read once, every tile
-  // pair computed once, spread evenly.
-  double total = 0;
-  for (const NItem& it : items) total += it.cost;
-  for (int32_t s = 0; s < nseg; ++s) {
-    if (!wide[s]) continue;
-    const int32_t G = m.seg_beam_end[s] - m.seg_beam_begin[s];
-    total += std::max(m.seg_nblocks[s] * blk_us, tiles_of(G * g) * ((m.seg_nblocks[s] + 1) / 2) * kTilePairUs / 4.0);
-  }
-  const double T = std::max(kMinUnitUs, total * hkv / (nbins * kUnitsPerBin));
-
-  // ---- templates (one per unit, before replication over KV heads) --------
+  // ---- units for a target unit time T ------------------------------------
   // A wide segment of G beams and n blocks is cut into C row chunks and P
   // pieces, in the wide mode (chunks of up to RW beams) or the narrow mode
   // (up to RB beams): the choice that moves the fewest bytes among those
-  // whose units fit the target time (else the fastest).
-  std::vector<Tmpl> tm;
-  int32_t ngroups = 0;
-  for (int32_t s = 0; s < nseg; ++s) {  // preorder: ancestors first
-    if (!wide[s]) continue;
-    const int32_t bb = m.seg_beam_begin[s], G = m.seg_beam_end[s] - bb;
-    const int32_t n = m.seg_nblocks[s], np = (n + 1) / 2;
-    struct Choice {
-      int32_t mode, C, P;
-      double bytes, us;
-    } best{kModeNarrow, 0, 0, 0, 0};
-    bool have = false, best_fits = false;
-    for (int32_t mode : {kModeWide, kModeNarrow}) {
-      if (mode == kModeWide && !wide_mode) continue;
-      const int32_t cap = mode == kModeWide ? RW : RB;
-      for (int32_t C = (G + cap - 1) / cap; C <= std::min(G, 4 * ((G + cap - 1) / cap)); ++C) {
-        const int32_t rows = ((G + C - 1) / C) * g;
-        for (int32_t P = std::max(1, (n + kMaxEntries - 1) / kMaxEntries); P <= np; ++P) {
-          const int32_t blocks = std::min(n, 2 * ((np + P - 1) / P));
-          const double us = mode == kModeWide ? cm.wide_us(blocks, rows) : cm.narrow_us(blocks, rows);
-          const double bytes = static_cast<double>(C) * P * cm.bytes(blocks, rows);
-          const bool fits = us <= T;
-          const bool better = !have || (fits && !best_fits) ||
-                              (fits == best_fits && (fits ? bytes < best.bytes : us < best.us));
-          if (better) {
-            best = {mode, C, P, bytes, us};
-            best_fits = fits;
-            have = true;
+  // whose units fit T (else the fastest). The narrow list is cut greedily
+  // into units that fit T.
+  auto make_templates = [&](double T, std::vector<Tmpl>& tm, int32_t& ngroups) {
+    tm.clear();
+    ngroups = 0;
+    for (int32_t s = 0; s < nseg; ++s) {  // preorder: ancestors first
+      if (!wide[s]) continue;
+      const int32_t bb = m.seg_beam_begin[s], G = m.seg_beam_end[s] - bb;
+      const int32_t n = m.seg_nblocks[s], np = (n + 1) / 2;
+      struct Choice {
+        int32_t mode, C, P;
+        double bytes, us;
+      } best{kModeNarrow, 0, 0, 0, 0};
+      bool have = false, best_fits = false;
+      for (int32_t mode : {kModeWide, kModeNarrow}) {
+        if (mode == kModeWide && !wide_mode) continue;
+        const int32_t cap = mode == kModeWide ? RW : RB;
+        for (int32_t C = (G + cap - 1) / cap; C <= std::min(G, 4 * ((G + cap - 1) / cap)); ++C) {
+          const int32_t rows = ((G + C - 1) / C) * g;
+          for (int32_t P = std::max(1, (n + kMaxEntries - 1) / kMaxEntries); P <= np; ++P) {
+            const int32_t blocks = std::min(n, 2 * ((np + P - 1) / P));
+            const double us = mode == kModeWide ? cm.wide_us(blocks, rows) : cm.narrow_us(blocks, rows);
+            const double bytes = static_cast<double>(C) * P * cm.bytes(blocks, rows);
+            const bool fits = us <= T;
+            const bool better = !have || (fits && !best_fits) ||
+                                (fits == best_fits && (fits ? bytes < best.bytes : us < best.us));
+            if (better) {
+              best = {mode, C, P, bytes, us};
+              best_fits = fits;
+              have = true;
+            }
+            if (fits) break;  // more pieces only add bytes
           }
-          if (fits) break;  // more pieces only add bytes
         }
       }
-    }
-    const int32_t C = best.C, pieces = best.P;
-    for (int32_t j = 0; j < pieces; ++j) {
-      const int32_t a = 2 * static_cast<int32_t>(static_cast<int64_t>(np) * j / pieces);
-      const int32_t e = std::min(n, 2 * static_cast<int32_t>(static_cast<int64_t>(np) * (j + 1) / pieces));
-      for (int32_t c = 0; c < C; ++c) {
-        Tmpl t;
-        t.lo = bb + static_cast<int32_t>(static_cast<int64_t>(G) * c / C);
-        t.hi = bb + static_cast<int32_t>(static_cast<int64_t>(G) * (c + 1) / C);
-        const int32_t rows = (t.hi - t.lo) * g;
-        t.mode = best.mode;
-        for (int32_t k = a; k < e; ++k) {
-          t.ids.push_back(seg_block(s, k));
-          t.info.push_back(t.mode == kModeWide ? 0u : ent_info(0, rows, bs, 0u));
+      const int32_t C = best.C, pieces = best.P;
+      for (int32_t j = 0; j < pieces; ++j) {
+        const int32_t a = 2 * static_cast<int32_t>(static_cast<int64_t>(np) * j / pieces);
+        const int32_t e = std::min(n, 2 * static_cast<int32_t>(static_cast<int64_t>(np) * (j + 1) / pieces));
+        for (int32_t c = 0; c < C; ++c) {
+          Tmpl t;
+          t.lo = bb + static_cast<int32_t>(static_cast<int64_t>(G) * c / C);
+          t.hi = bb + static_cast<int32_t>(static_cast<int64_t>(G) * (c + 1) / C);
+          const int32_t rows = (t.hi - t.lo) * g;
+          t.mode = best.mode;
+          for (int32_t k = a; k < e; ++k) {
+            t.ids.push_back(seg_block(s, k));
+            t.info.push_back(t.mode == kModeWide ? 0u : ent_info(0, rows, bs, 0u));
+          }
+          t.nstatic = e - a;
+          t.cost = t.mode == kModeWide ? cm.wide_us(e - a, rows) : cm.narrow_us(e - a, rows);
+          t.group = ngroups;
+          tm.push_back(std::move(t));
         }
-        t.nstatic = e - a;
-        t.cost = t.mode == kModeWide ? cm.wide_us(e - a, rows) : cm.narrow_us(e - a, rows);
-        t.group = ngroups;
-        tm.push_back(std::move(t));
+        ++ngroups;
       }
-      ++ngroups;
     }
-  }
-  {
     Tmpl cur;
-    std::vector<NItem> ext;
-    bool open = false;
+    std::vector<NItem> pend, ext;  // the open unit's static and extension items
+    int32_t nblk = 0;
     auto flush = [&]() {
-      if (!open) return;
+      if (pend.empty() && ext.empty()) return;
+      for (const NItem& it : pend) {
+        cur.ids.push_back(it.id);
+        cur.info.push_back(ent_info((it.p0 - cur.lo) * g, (it.p1 - cur.lo) * g, it.valid, it.flags));
+      }
+      cur.nstatic = static_cast<int32_t>(pend.size());
       for (const NItem& it : ext) {
         cur.ids.push_back(it.p0 - cur.lo);
         cur.info.push_back(ent_info((it.p0 - cur.lo) * g, (it.p1 - cur.lo) * g, 1, kEntExt));
@@ -262,41 +260,153 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
       cur.cost = cm.narrow_us(cur.nstatic, (cur.hi - cur.lo) * g);
       tm.push_back(std::move(cur));
       cur = Tmpl();
-      ext.clear();
-      open = false;
-    };
-    std::vector<NItem> pend;  // static items of the open unit (row offsets fixed at flush)
-    auto flush_all = [&]() {
-      if (!open) return;
-      for (const NItem& it : pend) {
-        cur.ids.push_back(it.id);
-        cur.info.push_back(ent_info((it.p0 - cur.lo) * g, (it.p1 - cur.lo) * g, it.valid, it.flags));
-      }
-      cur.nstatic = static_cast<int32_t>(pend.size());
       pend.clear();
-      flush();
+      ext.clear();
+      nblk = 0;
     };
     for (const NItem& it : items) {
-      if (open) {
+      const bool is_ext = (it.flags & kEntExt) != 0;
+      if (!pend.empty() || !ext.empty()) {
         const int32_t lo = std::min(cur.lo, it.p0), hi = std::max(cur.hi, it.p1);
         const bool fits = hi - lo <= RB && static_cast<int32_t>(pend.size() + ext.size()) + 1 <= kMaxEntries &&
-                          cur.cost + it.cost + cm.mem_us(0, (hi - lo) * g) + kUnitFixedUs <= T;
-        if (!fits) flush_all();
+                          cm.narrow_us(nblk + (is_ext ? 0 : 1), (hi - lo) * g) <= T;
+        if (!fits) flush();
       }
-      if (!open) {
-        open = true;
+      if (pend.empty() && ext.empty()) {
         cur.lo = it.p0;
         cur.hi = it.p1;
       }
       cur.lo = std::min(cur.lo, it.p0);
       cur.hi = std::max(cur.hi, it.p1);
-      cur.cost += it.cost;
-      if (it.flags & kEntExt)
+      if (is_ext) {
         ext.push_back(it);
-      else
+      } else {
         pend.push_back(it);
+        ++nblk;
+      }
     }
-    flush_all();
+    flush();
+  };
+
+  // ---- placement: groups -> XCDs -> workgroups ------------------------------
+  // Units are replicated per KV head. The wide chunks of one piece (same
+  // KV head) form a group that stays on one XCD, so they share its L2;
+  // groups go to the XCDs longest first, then each XCD's units to its
+  // workgroups longest first. Returns the largest workgroup load.
+  auto place = [&](const std::vector<Tmpl>& tm, int32_t ngroups, std::vector<std::vector<Work>>& bins) {
+    struct Group {
+      double cost = 0;
+      std::vector<Work> units;
+    };
+    std::vector<Group> groups;
+    std::vector<int32_t> gidx(static_cast<size_t>(ngroups) * hkv, -1);
+    for (int32_t kvh = 0; kvh < hkv; ++kvh) {
+      for (size_t t = 0; t < tm.size(); ++t) {
+        int32_t gi;
+        if (tm[t].group >= 0) {
+          int32_t& slot = gidx[static_cast<size_t>(tm[t].group) * hkv + kvh];
+          if (slot < 0) {
+            slot = static_cast<int32_t>(groups.size());
+            groups.emplace_back();
+          }
+          gi = slot;
+        } else {
+          gi = static_cast<int32_t>(groups.size());
+          groups.emplace_back();
+        }
+        groups[gi].units.push_back({static_cast<int32_t>(t), kvh, tm[t].cost});
+        groups[gi].cost += tm[t].cost;
+      }
+    }
+    std::vector<int32_t> gorder(groups.size());
+    std::iota(gorder.begin(), gorder.end(), 0);
+    std::stable_sort(gorder.begin(), gorder.end(),
+                     [&](int32_t a, int32_t b) { return groups[a].cost > groups[b].cost; });
+    const int32_t nx = std::min(kXcds, nbins);
+    std::vector<int32_t> xbins(nx, 0);
+    for (int32_t k = 0; k < nbins; ++k) xbins[k % nx]++;
+    std::vector<double> xload(nx, 0);
+    std::vector<std::vector<Work>> xunits(nx);
+    for (int32_t gi : gorder) {
+      int32_t x = 0;
+      for (int32_t k = 1; k < nx; ++k)
+        if (xload[k] / xbins[k] < xload[x] / xbins[x]) x = k;
+      xload[x] += groups[gi].cost;
+      for (const Work& w : groups[gi].units) xunits[x].push_back(w);
+    }
+    bins.assign(nbins, {});
+    double makespan = 0;
+    for (int32_t x = 0; x < nx; ++x) {
+      auto& v = xunits[x];
+      std::stable_sort(v.begin(), v.end(), [](const Work& a, const Work& b) { return a.cost > b.cost; });
+      std::vector<int32_t> mine;
+      for (int32_t k = x; k < nbins; k += nx) mine.push_back(k);
+      std::vector<double> load(mine.size(), 0);
+      for (const Work& w : v) {
+        size_t best = 0;
+        for (size_t k = 1; k < mine.size(); ++k)
+          if (load[k] < load[best]) best = k;
+        load[best] += w.cost;
+        bins[mine[best]].push_back(w);
+      }
+      for (double l : load) makespan = std::max(makespan, l);
+    }
+    // Within a workgroup, wide units first (their chunks run concurrently on
+    // the XCD's other workgroups and share its L2), then in creation order.
+    for (auto& v : bins)
+      std::stable_sort(v.begin(), v.end(), [](const Work& a, const Work& b) { return a.t < b.t; });
+    return makespan;
+  };
+
+  // ---- target search ---------------------------------------------------------
+  // Every unit pays a fixed cost and the kernel is bound by memory
+  // bandwidth shared by all workgroups, so the best plan has one unit per
+  // workgroup, all of about equal cost: the smallest target T whose units
+  // (times the KV heads) still fit in the workgroups (a binary search; the
+  // unit count only falls as T grows). When even the largest units
+  // outnumber the workgroups, units are chained, and the target with the
+  // smallest predicted makespan over a grid of candidates is taken.
+  double work = 0;
+  for (const NItem& it : items)
+    if (!(it.flags & kEntExt)) work += cm.narrow_us(1, 0) - kUnitFixedUs;
+  for (int32_t s = 0; s < nseg; ++s)
+    if (wide[s]) work += cm.wide_us(m.seg_nblocks[s], RW * g) - kUnitFixedUs;
+  work = work * hkv / nbins;
+  std::vector<Tmpl> tm;
+  std::vector<std::vector<Work>> bins;
+  int32_t ngroups = 0;
+  const int32_t fit_units = std::max(1, nbins / hkv);
+  auto units_at = [&](double T) {
+    make_templates(T, tm, ngroups);
+    return static_cast<int32_t>(tm.size());
+  };
+  double hi = kUnitFixedUs + 4.0 * work + 1.0;
+  if (units_at(hi) <= fit_units) {
+    double lo = kUnitFixedUs;
+    for (int it = 0; it < 24; ++it) {
+      const double mid = 0.5 * (lo + hi);
+      if (units_at(mid) <= fit_units)
+        hi = mid;
+      else
+        lo = mid;
+    }
+    units_at(hi);
+    place(tm, ngroups, bins);
+  } else {
+    std::vector<Tmpl> cand;
+    std::vector<std::vector<Work>> cbins;
+    double best = -1;
+    for (double f : {0.35, 0.5, 0.65, 0.8, 1.0, 1.2, 1.45, 1.75, 2.1, 2.5, 3.0, 4.0}) {
+      int32_t cg = 0;
+      make_templates(kUnitFixedUs + f * work, cand, cg);
+      const double ms = place(cand, cg, cbins);
+      if (best < 0 || ms < best) {
+        best = ms;
+        tm.swap(cand);
+        bins.swap(cbins);
+        ngroups = cg;
+      }
+    }
   }
 
   // ---- partial rows and merge lists ----------------------------------------
@@ -331,75 +441,6 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
     row[0] = static_cast<int32_t>(per_beam[b].size());
     std::copy(per_beam[b].begin(), per_beam[b].end(), row + 1);
   }
-
-  // ---- placement: groups -> XCDs -> workgroups ------------------------------
-  struct Work {
-    int32_t t, kvh;
-    double cost;
-  };
-  struct Group {
-    double cost = 0;
-    int32_t first = 0;  // creation order of its first unit (wide before narrow)
-    std::vector<Work> units;
-  };
-  std::vector<Group> groups;
-  {
-    std::vector<int32_t> gidx(static_cast<size_t>(ngroups) * hkv, -1);
-    for (int32_t kvh = 0; kvh < hkv; ++kvh) {
-      for (size_t t = 0; t < tm.size(); ++t) {
-        int32_t gi;
-        if (tm[t].group >= 0) {
-          int32_t& slot = gidx[static_cast<size_t>(tm[t].group) * hkv + kvh];
-          if (slot < 0) {
-            slot = static_cast<int32_t>(groups.size());
-            groups.emplace_back();
-            groups.back().first = static_cast<int32_t>(t);
-          }
-          gi = slot;
-        } else {
-          gi = static_cast<int32_t>(groups.size());
-          groups.emplace_back();
-          groups.back().first = static_cast<int32_t>(t);
-        }
-        groups[gi].units.push_back({static_cast<int32_t>(t), kvh, tm[t].cost});
-        groups[gi].cost += tm[t].cost;
-      }
-    }
-  }
-  std::vector<int32_t> gorder(groups.size());
-  std::iota(gorder.begin(), gorder.end(), 0);
-  std::stable_sort(gorder.begin(), gorder.end(), [&](int32_t a, int32_t b) { return groups[a].cost > groups[b].cost; });
-  const int32_t nx = std::min(kXcds, nbins);
-  std::vector<int32_t> xbins(nx, 0);
-  for (int32_t k = 0; k < nbins; ++k) xbins[k % nx]++;
-  std::vector<double> xload(nx, 0);
-  std::vector<std::vector<Work>> xunits(nx);
-  for (int32_t gi : gorder) {
-    int32_t x = 0;
-    for (int32_t k = 1; k < nx; ++k)
-      if (xload[k] / xbins[k] < xload[x] / xbins[x]) x = k;
-    xload[x] += groups[gi].cost;
-    for (const Work& w : groups[gi].units) xunits[x].push_back(w);
-  }
-  std::vector<std::vector<Work>> bins(nbins);
-  for (int32_t x = 0; x < nx; ++x) {
-    auto& v = xunits[x];
-    std::stable_sort(v.begin(), v.end(), [](const Work& a, const Work& b) { return a.cost > b.cost; });
-    std::vector<int32_t> mine;
-    for (int32_t k = x; k < nbins; k += nx) mine.push_back(k);
-    std::vector<double> load(mine.size(), 0);
-    for (const Work& w : v) {
-      size_t best = 0;
-      for (size_t k = 1; k < mine.size(); ++k)
-        if (load[k] < load[best]) best = k;
-      load[best] += w.cost;
-      bins[mine[best]].push_back(w);
-    }
-  }
-  // Within a workgroup, wide units first (their chunks run concurrently on
-  // the XCD's other workgroups and share its L2), then in creation order.
-  for (auto& v : bins)
-    std::stable_sort(v.begin(), v.end(), [](const Work& a, const Work& b) { return a.t < b.t; });
 
   // ---- records ---------------------------------------------------------------
   auto make_rec = [&](const Work& w) {

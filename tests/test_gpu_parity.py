@@ -72,6 +72,15 @@ def test_parity_straggler():
     assert err(op, ref) <= TOL["bf16"] and err(ox, ref) <= TOL["bf16"]
 
 
+def test_parity_balanced_tree():
+    """The low-sharing balanced tree (long private tails)."""
+    wl = make_workload("7b64_balanced", 0)
+    ref = oracle_attn_workload(wl)
+    op, ox = outputs(wl)
+    print(f"balanced: paged {err(op, ref):.2e} prefix {err(ox, ref):.2e}", flush=True)
+    assert err(op, ref) <= TOL["bf16"] and err(ox, ref) <= TOL["bf16"]
+
+
 def test_parity_longchain_fp8_sampled():
     wl = make_workload("7b_longchain_fp8", 0)
     s = wl.num_seqs

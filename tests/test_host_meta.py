@@ -53,7 +53,7 @@ def test_golden_example_matches():
     assert m["unique_tokens"] == exp["unique_tokens"] and m["unique_blocks"] == exp["unique_blocks"]
 
 
-@pytest.mark.parametrize("name", ["tiny", "1p5b16", "7b64", "7b_straggler"])
+@pytest.mark.parametrize("name", ["tiny", "1p5b16", "7b64", "7b64_balanced", "7b_straggler"])
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_configs_bit_exact(name, seed):
     cfg = CONFIGS[name]

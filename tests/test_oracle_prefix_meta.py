@@ -130,7 +130,7 @@ def test_config_trees(name, seed):
     check_meta(w.req_seq_offsets, w.block_tables, w.seq_lens, m)
 
 
-@pytest.mark.parametrize("name", ["7b64", "7b_straggler"])
+@pytest.mark.parametrize("name", ["7b64", "7b64_balanced", "7b_straggler"])
 def test_unique_tokens_two_ways(name):
     """unique_tokens/blocks from the metadata == recount from the generator's allocation records."""
     cfg = CONFIGS[name]

@@ -60,7 +60,10 @@ class ReqSpec:
     stops: ``"lmax"`` stops before an iteration whose full step could push
     the longest beam past ``max_len`` or once ``max_iters`` is reached;
     ``"fixed"`` runs ``round((target_median - prompt) / fixed_div)`` (at
-    least 1) full iterations. The last iteration is the snapshot:
+    least 1) full iterations; ``"balanced"`` grows a complete tree instead
+    (every beam of a level forks ``branch`` children, one step per level,
+    until ``beams`` leaves) and then gives every leaf a private tail to a
+    total length U[max_len / 2, max_len]. The last iteration is the snapshot:
     ``"none"`` appends the full step, ``"uniform"`` appends U[1, step],
     ``"lognormal"`` sets the beam's total length to
     ``clip(lognormal(ln median, sigma), len + 1, max_len)``.
@@ -112,6 +115,13 @@ CONFIGS = {
         AttnShape(28, 4, 128, 16, "bf16", "bf16"),
         (ReqSpec(beams=64, branch=4, prompt=(1024, 1024), step=(64, 256), max_len=4096),),
         "7B-shaped: Hq28/Hkv4, D128, bf16 KV, 64 beams, 1024-token prompt, branch 4, steps U[64,256], len<=4096",
+    ),
+    "7b64_balanced": WorkloadConfig(
+        "7b64_balanced",
+        AttnShape(28, 4, 128, 16, "bf16", "bf16"),
+        (ReqSpec(beams=64, branch=4, prompt=(1024, 1024), step=(64, 256), max_len=4096, rule="balanced"),),
+        "7B-shaped balanced tree (report only): 1024-token prompt -> 4 -> 16 -> 64 nodes of one U[64,256] step, "
+        "then private tails to U[2048,4096] tokens, bf16 KV",
     ),
     "7b_straggler": WorkloadConfig(
         "7b_straggler",
@@ -199,6 +209,28 @@ def _grow_request(tree: BeamTree, rng: np.random.Generator, spec: ReqSpec) -> No
     parents: List[int] = []
     it = 0
     lo, hi = spec.step
+    if spec.rule == "balanced":
+        beams = [(_fork(tree, prompt_blocks, p_len), p_len) for _ in range(br)]
+        parents = [-1] * br
+        while True:
+            steps = rng.integers(lo, hi + 1, size=len(beams))
+            beams = [(b, _append(tree, b, ln, int(s))) for (b, ln), s in zip(beams, steps)]
+            if len(beams) * br > n:
+                break
+            kids, kid_parent = [], []
+            for i, (b, ln) in enumerate(beams):
+                for _ in range(br):
+                    kids.append((_fork(tree, b, ln), ln))
+                    kid_parent.append(i)
+            beams, parents = kids, kid_parent
+        for (b, ln), par in zip(beams, parents):
+            tot = int(rng.integers(spec.max_len // 2, spec.max_len + 1))
+            ln = _append(tree, b, ln, max(1, tot - ln))
+            tree.beam_allocs.append(b)
+            tree.beam_lens.append(ln)
+            tree.beam_parent.append(par)
+        tree.req_offsets.append(len(tree.beam_lens))
+        return
     while True:
         it += 1
         if it == 1:
