@@ -416,7 +416,7 @@ __device__ __forceinline__ void tile_step(const Ops<D, KV>& f, const QFrag<D, KV
 // wave reads all chunks. (Plain loads stream faster than global-to-LDS
 // copies here.)
 template <int D, int KV>
-struct Stage {  // meaningful for bf16 caches (the only ones with wide units)
+struct Stage {  // bf16 operands (fp8 caches stage their codes converted)
   static constexpr int kKChunks = 2 * (D / 32);
   static constexpr int kChunks = kKChunks + D / 16;
   static constexpr int kPerWave = kChunks / kWaves;
@@ -433,16 +433,19 @@ __device__ __forceinline__ const unsigned char* frag_src(int c, const unsigned c
   if (c < S::kKChunks) {
     const int t = c / (D / 32), j = c % (D / 32);
     const int tok = pair_token(t, ln);
-    return (tok < 16 ? kb0 : kb1) + (tok & 15) * G::row_bytes + (4 * j + lq) * 16;
+    return (tok < 16 ? kb0 : kb1) + (tok & 15) * G::row_bytes + (KV == kKvFp8 ? 32 * j + 8 * lq : (4 * j + lq) * 16);
   }
   const int dt = c - S::kKChunks;
   return (lq >= 2 ? vb1 : vb0) + (lq & 1) * 8 * G::eb + ln * G::vrow_bytes + 16 * dt * G::vrow_bytes;
 }
 
 // (A vector value rather than an array, so that it stays in registers.)
+// fp8 caches hold the raw codes (8 bytes per fragment) until the quarter is
+// stored, converted, to the stage.
 template <int D, int KV>
 struct Quarter {
-  typedef unsigned int V __attribute__((ext_vector_type(4 * Stage<D, KV>::kPerWave)));
+  static constexpr int kWords = KV == kKvFp8 ? 2 : 4;  // dwords per fragment
+  typedef unsigned int V __attribute__((ext_vector_type(kWords * Stage<D, KV>::kPerWave)));
   V v;
 };
 
@@ -457,20 +460,32 @@ __device__ __forceinline__ void load_quarter(Quarter<D, KV>& q, int id0, int id1
   const unsigned char* vb1 = vbase + id1 * blk_stride;
 #pragma unroll
   for (int i = 0; i < S::kPerWave; ++i) {
-    const uint4 t = *reinterpret_cast<const uint4*>(frag_src<D, KV>(wave + kWaves * i, kb0, kb1, vb0, vb1, ln, lq));
-    q.v[4 * i] = t.x;
-    q.v[4 * i + 1] = t.y;
-    q.v[4 * i + 2] = t.z;
-    q.v[4 * i + 3] = t.w;
+    const unsigned char* src = frag_src<D, KV>(wave + kWaves * i, kb0, kb1, vb0, vb1, ln, lq);
+    if constexpr (KV == kKvFp8) {
+      const uint2 t = *reinterpret_cast<const uint2*>(src);
+      q.v[2 * i] = t.x;
+      q.v[2 * i + 1] = t.y;
+    } else {
+      const uint4 t = *reinterpret_cast<const uint4*>(src);
+      q.v[4 * i] = t.x;
+      q.v[4 * i + 1] = t.y;
+      q.v[4 * i + 2] = t.z;
+      q.v[4 * i + 3] = t.w;
+    }
   }
 }
 
 template <int D, int KV>
 __device__ __forceinline__ void store_quarter(const Quarter<D, KV>& q, unsigned char* stage, int wave, int lane) {
 #pragma unroll
-  for (int i = 0; i < Stage<D, KV>::kPerWave; ++i)
-    *reinterpret_cast<uint4*>(stage + (wave + kWaves * i) * 1024 + lane * 16) =
-        uint4{q.v[4 * i], q.v[4 * i + 1], q.v[4 * i + 2], q.v[4 * i + 3]};
+  for (int i = 0; i < Stage<D, KV>::kPerWave; ++i) {
+    uint4 w;
+    if constexpr (KV == kKvFp8)
+      w = fp8x8_to_bf16x8(uint2{q.v[2 * i], q.v[2 * i + 1]});
+    else
+      w = uint4{q.v[4 * i], q.v[4 * i + 1], q.v[4 * i + 2], q.v[4 * i + 3]};
+    *reinterpret_cast<uint4*>(stage + (wave + kWaves * i) * 1024 + lane * 16) = w;
+  }
 }
 
 template <int D, int KV>
@@ -691,7 +706,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
   // Wide units (bf16) use the area after the query rows for their pair
   // stages instead.
   constexpr int kCombBytes = kWaves * (kTiles - 1) * G::comb_floats * 4;
-  constexpr int kStageBytes = KV == kKvBf16 ? 2 * Stage<D, KV>::bytes : 0;
+  constexpr int kStageBytes = KV != kKvF32 ? 2 * Stage<D, KV>::bytes : 0;
   constexpr int kAreaBytes = kCombBytes > kStageBytes ? kCombBytes : kStageBytes;
   __shared__ __attribute__((aligned(16))) unsigned char lds[Q::bytes + kAreaBytes];
   unsigned char* qbuf = lds;
@@ -773,7 +788,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
     const unsigned char* kbase = static_cast<const unsigned char*>(p.k_cache) + kvh * G::blk_bytes;
     const unsigned char* vbase = static_cast<const unsigned char*>(p.v_cache) + kvh * G::blk_bytes;
 
-    if constexpr (KV == kKvBf16) {
+    if constexpr (KV != kKvF32) {
       if (rfl(u.mode) == kModeWide) {
         // ---- wide unit: wave w owns row tiles w, w + 4, ...; every block
         // pair is copied to an LDS stage once and read by all four waves ---
@@ -815,13 +830,24 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             st[i].seen = kNegInf;
           }
           Quarter<D, KV> qa, qb;
+          // fp8: the pair's block scales (K of block 0, 1; V of block 0, 1),
+          // loaded with its quarter.
+          f32x4 sa, sb;
+          auto scales = [&](int i0, int i1) {
+            if constexpr (KV == kKvFp8)
+              return f32x4{p.k_scale[i0], p.k_scale[i1], p.v_scale[i0], p.v_scale[i1]};
+            else
+              return f32x4{1.f, 1.f, 1.f, 1.f};
+          };
           int id0, id1;
           pair_ids(0, &id0, &id1);
           load_quarter<D, KV>(qa, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
+          sa = scales(id0, id1);
           __syncthreads();  // every wave is done with the stage area (previous unit or attempt)
-          auto step = [&](Quarter<D, KV>& cur, Quarter<D, KV>& nxt, int pp) {
+          auto step = [&](Quarter<D, KV>& cur, Quarter<D, KV>& nxt, const f32x4& cs, f32x4& ns, int pp) {
             pair_ids(pp + 1, &id0, &id1);
             load_quarter<D, KV>(nxt, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
+            ns = scales(id0, id1);
             unsigned char* stage = stages + (pp & 1) * SG::bytes;
             store_quarter<D, KV>(cur, stage, wave, lane);
             __syncthreads();  // the whole pair is in the stage
@@ -832,8 +858,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             pi.v1 = 2 * pp + 1 < nst ? kTok : 0;
             pi.a0 = pi.a1 = 0;
             pi.e0 = pi.e1 = nrows;
-            pi.ks0 = pi.ks1 = sc_w;
-            pi.vs0 = pi.vs1 = 1.f;
+            pi.ks0 = sc_w * cs.x;
+            pi.ks1 = sc_w * cs.y;
+            pi.vs0 = cs.z;
+            pi.vs1 = cs.w;
             if (pi.v1 == 0) mask_v<D, KV>(o, lq, pi.v0, pi.v1);
             // The unit's tiles per wave (uniform): one straight-line block
             // per count, so the compiler interleaves the tiles' products.
@@ -848,9 +876,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             }
           };
           for (int pp = 0; pp < np; pp += 2) {
-            step(qa, qb, pp);
+            step(qa, qb, sa, sb, pp);
             if (pp + 1 >= np) break;
-            step(qb, qa, pp + 1);
+            step(qb, qa, sb, sa, pp + 1);
           }
           if (attempt == 0) TTS_PROF_MARK(1, rec_idx);
           if (attempt > 0) break;

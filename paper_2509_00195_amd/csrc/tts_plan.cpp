@@ -11,7 +11,7 @@
 //   kMaxWideRows rows: the four waves of the workgroup share every block
 //   through LDS, each taking a quarter of the row tiles) and, along its
 //   blocks, into pieces; every (piece, chunk) is a unit whose blocks apply
-//   to all of its rows. (fp32 and fp8 caches use chunks of kMaxRows rows.) The
+//   to all of its rows. (fp32 caches use chunks of kMaxRows rows.) The
 //   chunks of one piece read the same blocks and are placed on one XCD.
 // * Narrow units. Everything else -- segments of few beams and every beam's
 //   private tail -- is listed depth-first over the prefix tree (a segment's
@@ -99,8 +99,8 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
   const int32_t hkv = shape.num_kv_heads;
   const int32_t bs = m.block_size;
   const int32_t RB = std::max(1, std::min(kMaxUnitBeams, kMaxRows / g));  // beams per narrow unit
-  // Beams per wide unit (bf16 caches; fp32 and fp8 caches use narrow-sized chunks).
-  const bool wide_mode = shape.kv_bytes == 2;
+  // Beams per wide unit (bf16 and fp8 caches; fp32 caches use narrow-sized chunks).
+  const bool wide_mode = shape.kv_bytes <= 2;
   const int32_t RW = wide_mode ? std::max(1, std::min(kMaxWideBeams, kMaxWideRows / g)) : RB;
   const int32_t nseg = static_cast<int32_t>(m.seg_req.size());
   const int32_t nbins = std::max(1, shape.num_bins);
