@@ -37,14 +37,17 @@ namespace {
 // fitted to per-unit clock marks of the kernel at the 7B-shaped 64-beam
 // tree (D 128, bf16 KV, g 7): every unit pays a fixed part (its first
 // memory round trips, the end of its loop, the partial writes); a narrow
-// unit then streams its blocks at about 0.166 us per 8 KiB block and pays
-// about 0.064 us per query row (query read, combine, partial state); a wide
+// unit then streams its blocks at about 0.21 us per 8 KiB block and pays
+// about 0.08 us per query row (query read, combine, partial state); a wide
 // unit pays about 0.193 us per 8 KiB block for staging it through LDS plus
-// 0.113 us per block for each row tile a wave runs. Other shapes scale the
-// block terms by their bytes and the tile term by the head size.
+// 0.113 us per block for each row tile a wave runs. (The narrow terms are
+// the least-squares fit scaled by 1.25: a plain fit under-predicts the
+// largest narrow units, which then finish last; the scale was chosen by
+// timing the kernel.) Other shapes scale the block terms by their bytes and
+// the tile term by the head size.
 constexpr double kUnitFixedUs = 4.9;
-constexpr double kNarrowUsPerByte = 0.166 / 8192;
-constexpr double kRowUs = 0.064;  // per row of 256 + 272 bytes (query + partial state)
+constexpr double kNarrowUsPerByte = 0.2075 / 8192;
+constexpr double kRowUs = 0.08;  // per row of 256 + 272 bytes (query + partial state)
 constexpr double kWideUsPerByte = 0.193 / 8192;
 constexpr double kTileBlockUs = 0.113;  // per block and row tile of a wave, D = 128
 constexpr int kXcds = 8;  // workgroup k of a launch runs on XCD k % 8
