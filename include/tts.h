@@ -224,6 +224,64 @@ tts_status tts_prefix_decode_partials(const tts_attn_desc* d, const tts_prefix_m
 tts_status tts_prefix_decode_merge(const tts_attn_desc* d, const tts_prefix_meta* m, const int32_t* seq_lens,
                                    void* out, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* ---- KV-cache maintenance around the decode step ---------------------------
+ *
+ * A decode step writes each beam's new token into the paged cache before the
+ * attention reads it (seq_len counts it), and the search's duplication step
+ * (DuplicateThenTruncate, Sec. 3.1 and Alg. 1: surviving beams are
+ * duplicated; the duplicates' speculative tokens are truncated, Sec. 4.1)
+ * shares a parent's full blocks with its children and copies the partially
+ * filled block each child keeps (copy-on-write). */
+
+/* Append: for every beam b with L = seq_lens[b] > 0, store its token at
+ * position L - 1 (slot (L - 1) % 16 of block block_tables[b][(L - 1) / 16]):
+ * k_new[b][h][:] into that block's K row of KV head h, v_new[b][h][:] into
+ * its V column. k_new, v_new: [num_seqs][Hkv][D] device arrays, bf16 for
+ * BF16 and FP8_E4M3 caches, fp32 for F32 caches. Beams with seq_len 0, a
+ * block index past their table row or a block id outside [0, num_blocks)
+ * write nothing.
+ * FP8 caches (k_scale/v_scale required): each of K and V is stored as
+ * E4M3FN codes of value / scale[block] (round to nearest even, saturating
+ * at 448). A token opening a block (slot 0) sets the block's scale to
+ * amax / 448 over the token's values of all KV heads (1 if all are zero);
+ * a later token whose amax exceeds 448 * scale raises the scale to
+ * amax / 448 and re-encodes the block's earlier codes of every head under
+ * it (decode * old scale / new scale); otherwise the scale is kept.
+ * Every beam's current block must belong to that beam alone (a shared
+ * partial block is copied first, see tts_fork_tables); beams writing the
+ * same block in one call race. */
+tts_status tts_append_kv(const tts_attn_desc* d, int32_t num_seqs, const void* k_new, const void* v_new,
+                         const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                         int32_t num_blocks, void* k_cache, void* v_cache, float* k_scale, float* v_scale,
+                         hipStream_t stream);
+
+/* Copy whole blocks: for each i < num_pairs, K and V of every KV head of
+ * block pairs[2i] into block pairs[2i + 1] (and the fp8 scales). pairs is a
+ * device int32 array. Pairs naming a block outside [0, num_blocks), or a
+ * block onto itself, copy nothing. Destinations must be distinct and not
+ * be sources of the same call. */
+tts_status tts_copy_blocks(const tts_attn_desc* d, int32_t num_pairs, const int32_t* pairs, int32_t num_blocks,
+                           void* k_cache, void* v_cache, float* k_scale, float* v_scale, hipStream_t stream);
+
+/* Host: block tables of duplicated beams. Child c copies the first
+ * child_lens[c] tokens of beam child_parent[c] (0 <= child_lens[c] <=
+ * parent length; a shorter child drops its parent's speculative tokens).
+ * Its full blocks are its parent's (shared, same ids); a partially filled
+ * last block becomes the next id of free_ids, and the pair (parent's
+ * block, new id) is appended to copies ([num_children][2] capacity) for
+ * tts_copy_blocks. Entries past the child's blocks are -1. All arrays are
+ * host int32: parent_tables [num_parents][max_blocks_per_seq],
+ * child_tables [num_children][max_blocks_per_seq] (written). Outputs the
+ * number of copies and of free ids consumed (in order). Errors
+ * (TTS_ERR_OUT_OF_RANGE for a bad parent index, TTS_ERR_INVALID_ARG for a
+ * bad length, TTS_ERR_NOMEM when free_ids runs out) are detected before
+ * anything is written. */
+tts_status tts_fork_tables(int32_t num_parents, const int32_t* parent_tables, int32_t max_blocks_per_seq,
+                           const int32_t* parent_lens, int32_t block_size, int32_t num_children,
+                           const int32_t* child_parent, const int32_t* child_lens, const int32_t* free_ids,
+                           int32_t num_free, int32_t* child_tables, int32_t* copies, int32_t* num_copies,
+                           int32_t* num_free_used);
+
 /* Thread-local text of the last error ("" if none). */
 const char* tts_last_error(void);
 

@@ -12,7 +12,10 @@ from .tts import (  # noqa: F401
     PrefixMeta,
     load,
     make_desc,
+    tts_append_kv,
     tts_build_prefix_meta,
+    tts_copy_blocks,
+    tts_fork_tables,
     tts_paged_decode_attn,
     tts_paged_decode_workspace_size,
     tts_prefix_decode_attn,

@@ -17,6 +17,11 @@
 namespace tts {
 hipError_t launch_attn(const AttnParams& p, int grid, int head_dim, int kv_kind, hipStream_t stream);
 hipError_t launch_merge(const MergeParams& p, int head_dim, int kv_kind, hipStream_t stream);
+hipError_t launch_append(const void* k_new, const void* v_new, const int32_t* block_tables, const int32_t* seq_lens,
+                         void* k_cache, void* v_cache, float* k_scale, float* v_scale, int num_seqs, int max_blocks,
+                         int num_blocks, int hkv, int head_dim, int kv_kind, hipStream_t stream);
+hipError_t launch_copy_blocks(const int32_t* pairs, int num_pairs, void* k_cache, void* v_cache, float* k_scale,
+                              float* v_scale, int64_t blk_bytes, int num_blocks, hipStream_t stream);
 }  // namespace tts
 
 namespace {
@@ -421,6 +426,83 @@ tts_status tts_prefix_decode_merge(const tts_attn_desc* d, const tts_prefix_meta
                                workspace, workspace_bytes, false, &p);
   if (s != TTS_OK || m->host.num_seqs == 0) return s == TTS_OK ? ok() : s;
   if ((s = launch_prefix_merge(d, m, p, stream)) != TTS_OK) return s;
+  return ok();
+}
+
+// ---- KV maintenance ----------------------------------------------------------
+
+tts_status tts_append_kv(const tts_attn_desc* d, int32_t num_seqs, const void* k_new, const void* v_new,
+                         const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                         int32_t num_blocks, void* k_cache, void* v_cache, float* k_scale, float* v_scale,
+                         hipStream_t stream) {
+  tts_status s = check_desc(d);
+  if (s != TTS_OK) return s;
+  if ((s = check_scales(d, k_scale, v_scale)) != TTS_OK) return s;
+  if (num_seqs < 0 || max_blocks_per_seq < 0 || num_blocks < 0) return fail(TTS_ERR_INVALID_ARG, "negative size");
+  if (num_seqs == 0) return ok();
+  if (!k_new || !v_new || !block_tables || !seq_lens || !k_cache || !v_cache)
+    return fail(TTS_ERR_INVALID_ARG, "NULL device pointer");
+  hipError_t e = tts::launch_append(k_new, v_new, block_tables, seq_lens, k_cache, v_cache, k_scale, v_scale, num_seqs,
+                                    max_blocks_per_seq, num_blocks, d->num_kv_heads, d->head_dim, kv_kind(d), stream);
+  if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("append launch: ") + hipGetErrorString(e));
+  return ok();
+}
+
+tts_status tts_copy_blocks(const tts_attn_desc* d, int32_t num_pairs, const int32_t* pairs, int32_t num_blocks,
+                           void* k_cache, void* v_cache, float* k_scale, float* v_scale, hipStream_t stream) {
+  tts_status s = check_desc(d);
+  if (s != TTS_OK) return s;
+  if ((s = check_scales(d, k_scale, v_scale)) != TTS_OK) return s;
+  if (num_pairs < 0 || num_blocks < 0) return fail(TTS_ERR_INVALID_ARG, "negative size");
+  if (num_pairs == 0) return ok();
+  if (!pairs || !k_cache || !v_cache) return fail(TTS_ERR_INVALID_ARG, "NULL device pointer");
+  const int64_t eb = d->kv_dtype == TTS_F32 ? 4 : (d->kv_dtype == TTS_BF16 ? 2 : 1);
+  const int64_t blk_bytes = static_cast<int64_t>(d->num_kv_heads) * d->block_size * d->head_dim * eb;
+  hipError_t e = tts::launch_copy_blocks(pairs, num_pairs, k_cache, v_cache, k_scale, v_scale, blk_bytes, num_blocks,
+                                         stream);
+  if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("copy launch: ") + hipGetErrorString(e));
+  return ok();
+}
+
+tts_status tts_fork_tables(int32_t num_parents, const int32_t* parent_tables, int32_t max_blocks_per_seq,
+                           const int32_t* parent_lens, int32_t block_size, int32_t num_children,
+                           const int32_t* child_parent, const int32_t* child_lens, const int32_t* free_ids,
+                           int32_t num_free, int32_t* child_tables, int32_t* copies, int32_t* num_copies,
+                           int32_t* num_free_used) {
+  if (num_parents < 0 || num_children < 0 || max_blocks_per_seq < 0 || num_free < 0 || block_size <= 0)
+    return fail(TTS_ERR_INVALID_ARG, "negative size");
+  if (!num_copies || !num_free_used) return fail(TTS_ERR_INVALID_ARG, "NULL output count");
+  *num_copies = 0;
+  *num_free_used = 0;
+  if (num_children == 0) return ok();
+  if (!child_parent || !child_lens || !child_tables || !copies || (num_parents > 0 && (!parent_tables || !parent_lens)))
+    return fail(TTS_ERR_INVALID_ARG, "NULL host array");
+  // Validate everything before writing anything.
+  int32_t need = 0;
+  for (int32_t c = 0; c < num_children; ++c) {
+    const int32_t par = child_parent[c];
+    if (par < 0 || par >= num_parents) return fail(TTS_ERR_OUT_OF_RANGE, "child_parent outside [0, num_parents)");
+    const int32_t pl = parent_lens[par], cl = child_lens[c];
+    if (pl < 0 || static_cast<int64_t>(pl) > static_cast<int64_t>(max_blocks_per_seq) * block_size)
+      return fail(TTS_ERR_INVALID_ARG, "parent length outside [0, max_blocks_per_seq * block_size]");
+    if (cl < 0 || cl > pl) return fail(TTS_ERR_INVALID_ARG, "child length outside [0, parent length]");
+    if (cl % block_size) ++need;
+  }
+  if (need > num_free) return fail(TTS_ERR_NOMEM, "not enough free blocks for the copied partial blocks");
+  for (int32_t c = 0; c < num_children; ++c) {
+    const int32_t par = child_parent[c], cl = child_lens[c];
+    const int32_t* prow = parent_tables + static_cast<int64_t>(par) * max_blocks_per_seq;
+    int32_t* crow = child_tables + static_cast<int64_t>(c) * max_blocks_per_seq;
+    const int32_t full = cl / block_size;
+    for (int32_t j = 0; j < max_blocks_per_seq; ++j) crow[j] = j < full ? prow[j] : -1;
+    if (cl % block_size) {
+      const int32_t dst = free_ids[(*num_free_used)++];
+      crow[full] = dst;
+      copies[2 * *num_copies] = prow[full];
+      copies[2 * *num_copies + 1] = dst;
+      ++*num_copies;
+    }
+  }
   return ok();
 }
 

@@ -35,7 +35,7 @@ EXPORTED = [
     "tts_build_prefix_meta", "tts_prefix_meta_destroy", "tts_prefix_meta_export", "tts_prefix_meta_coverage",
     "tts_prefix_meta_stats", "tts_paged_decode_workspace_size", "tts_paged_decode_attn",
     "tts_prefix_decode_workspace_size", "tts_prefix_decode_attn", "tts_prefix_decode_partials",
-    "tts_prefix_decode_merge", "tts_last_error",
+    "tts_prefix_decode_merge", "tts_append_kv", "tts_copy_blocks", "tts_fork_tables", "tts_last_error",
 ]
 
 
@@ -105,6 +105,12 @@ def load() -> C.CDLL:
     lib.tts_prefix_decode_partials.argtypes = lib.tts_prefix_decode_attn.argtypes
     lib.tts_prefix_decode_merge.restype = C.c_int
     lib.tts_prefix_decode_merge.argtypes = [P(tts_attn_desc), VP, VP, VP, VP, C.c_size_t, VP]
+    lib.tts_append_kv.restype = C.c_int
+    lib.tts_append_kv.argtypes = [P(tts_attn_desc), I32, VP, VP, VP, I32, VP, I32, VP, VP, VP, VP, VP]
+    lib.tts_copy_blocks.restype = C.c_int
+    lib.tts_copy_blocks.argtypes = [P(tts_attn_desc), I32, VP, I32, VP, VP, VP, VP, VP]
+    lib.tts_fork_tables.restype = C.c_int
+    lib.tts_fork_tables.argtypes = [I32, pi32, I32, pi32, I32, I32, pi32, pi32, pi32, I32, pi32, pi32, pi32, pi32]
     _lib = lib
     return lib
 
@@ -273,3 +279,33 @@ def tts_prefix_decode_merge(desc: tts_attn_desc, meta: PrefixMeta, seq_lens, out
                             stream=None):
     _check(load().tts_prefix_decode_merge(C.byref(desc), meta.handle, _ptr(seq_lens), _ptr(out), _ptr(workspace),
                                           workspace_bytes, _stream(stream)))
+
+
+def tts_append_kv(desc: tts_attn_desc, num_seqs: int, k_new, v_new, block_tables, max_blocks_per_seq: int, seq_lens,
+                  num_blocks: int, k_cache, v_cache, k_scale=None, v_scale=None, stream=None):
+    _check(load().tts_append_kv(
+        C.byref(desc), num_seqs, _ptr(k_new), _ptr(v_new), _ptr(block_tables), max_blocks_per_seq, _ptr(seq_lens),
+        num_blocks, _ptr(k_cache), _ptr(v_cache), _ptr(k_scale), _ptr(v_scale), _stream(stream)))
+
+
+def tts_copy_blocks(desc: tts_attn_desc, num_pairs: int, pairs, num_blocks: int, k_cache, v_cache, k_scale=None,
+                    v_scale=None, stream=None):
+    _check(load().tts_copy_blocks(C.byref(desc), num_pairs, _ptr(pairs), num_blocks, _ptr(k_cache), _ptr(v_cache),
+                                  _ptr(k_scale), _ptr(v_scale), _stream(stream)))
+
+
+def tts_fork_tables(parent_tables, parent_lens, block_size: int, child_parent, child_lens, free_ids):
+    """Host call; returns (child_tables [C][max_blocks], copies [n][2], number of free ids used)."""
+    lib = load()
+    pt = _host_i32(parent_tables)
+    if pt.ndim != 2:
+        pt = pt.reshape(-1, 0) if pt.size == 0 else pt.reshape(1, -1)
+    pl, cp, cl, fr = _host_i32(parent_lens), _host_i32(child_parent), _host_i32(child_lens), _host_i32(free_ids)
+    nc, mb = cp.shape[0], pt.shape[1]
+    ct = np.zeros((max(nc, 1), max(mb, 1)), np.int32)
+    cps = np.zeros((max(nc, 1), 2), np.int32)
+    ncp, nfu = C.c_int32(0), C.c_int32(0)
+    _check(lib.tts_fork_tables(pt.shape[0], _as_i32p(pt), mb, _as_i32p(pl), block_size, nc, _as_i32p(cp),
+                               _as_i32p(cl), _as_i32p(fr), fr.shape[0], _as_i32p(ct), _as_i32p(cps),
+                               C.byref(ncp), C.byref(nfu)))
+    return ct[:nc, :mb], cps[: ncp.value], nfu.value
