@@ -271,6 +271,38 @@ def main():
     kv_bytes = unique_kv if args.variant == "prefix" else logical_kv
     achieved = kv_bytes / (kms * 1e-3) / 1e9
 
+    # The KV steps around the call, on layer 0's pool: appending every beam's
+    # token (tts_append_kv) and the copy-on-write copies of a duplication
+    # step (tts_copy_blocks, one partial block per beam).
+    q0, k0, v0, ks0, vs0 = pools[0]
+    kv_src = torch.zeros((wl.num_seqs, sh.num_kv_heads, sh.head_dim),
+                         dtype=torch.float32 if sh.kv_dtype == "f32" else torch.bfloat16, device=dev)
+    kv_src.normal_()
+    # (Timed as replays of a captured HIP graph of 50 calls: eager, each call
+    # is bound by the host's launch path, not by the GPU.)
+    def graph_ms(call, reps=50):
+        call()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for _ in range(reps):
+                call()
+        g.replay()
+        return timed(lambda n: [g.replay() for _ in range(n)], 4) / (4 * reps)
+
+    append_ms = graph_ms(lambda: T.tts_append_kv(pref.desc, wl.num_seqs, kv_src, kv_src, tabs, maxb, lens,
+                                                 wl.num_blocks, k0, v0, ks0, vs0, stream))
+    used = set()
+    src_ids = []
+    for b in range(wl.num_seqs):
+        nblk = -(-int(wl.seq_lens[b]) // 16)
+        used.update(wl.block_tables[b, :nblk].tolist())
+        src_ids.append(int(wl.block_tables[b, max(nblk - 1, 0)]))
+    spare = [i for i in range(wl.num_blocks) if i not in used][: wl.num_seqs]
+    pairs = torch.tensor(list(zip(src_ids, spare)), dtype=torch.int32, device=dev).reshape(-1, 2).contiguous()
+    copy_ms = graph_ms(lambda: T.tts_copy_blocks(pref.desc, int(pairs.shape[0]), pairs, wl.num_blocks, k0, v0, ks0,
+                                                 vs0, stream))
+
     # Streaming calibration on the same GPU: an elementwise copy of 1 GiB
     # (dst = ~src), one read and one write per byte, timed the same way.
     csrc = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
@@ -313,6 +345,8 @@ def main():
             "sharing": logical_kv / max(unique_kv, 1),
             "unique_kv_hbm_frac_per_call": unique_kv / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
             "stream_copy_gbs": stream_gbs,
+            "append_kv_us": append_ms * 1e3,
+            "copy_blocks_us": copy_ms * 1e3,
             "attention_frac_of_stream_copy": achieved / stream_gbs,
             "attention_kernel_us": kms * 1e3,
             "merge_and_gaps_us": (ms_per_step - kms) * 1e3,
