@@ -12,6 +12,10 @@ slow and written to be checked by eye against its definitions:
   spawned from the same parent are adjacent while the parents keep their
   relative order (Sec. 4.2, Dynamic Prefix-Aware Scheduling).
 * ``fp8.e4m3_table`` -- the 256 OCP E4M3FN code values from the bit formula.
+* ``kv_ops`` -- the KV-cache steps around decode: E4M3 encoding by nearest
+  table value, appending each beam's token (with the fp8 block-scale rule),
+  block copies, and the block tables of duplicated beams
+  (DuplicateThenTruncate, Sec. 3.1 and Alg. 1).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package. The product path (the HIP library and
@@ -26,4 +30,5 @@ routine or hand-derived golden fixtures.
 
 from .attention import decode_bf16, oracle_attn, oracle_attn_row  # noqa: F401
 from .fp8 import e4m3_table  # noqa: F401
+from .kv_ops import append_kv, copy_blocks, e4m3_encode, fork_tables  # noqa: F401
 from .prefix_meta import oracle_coverage, oracle_prefix_meta  # noqa: F401
