@@ -282,6 +282,54 @@ tts_status tts_fork_tables(int32_t num_parents, const int32_t* parent_tables, in
                            int32_t num_free, int32_t* child_tables, int32_t* copies, int32_t* num_copies,
                            int32_t* num_free_used);
 
+/* ---- Roofline-guided KV allocation (Sec. 4.3) -------------------------------
+ *
+ * Split one KV-cache budget M between the verifier (prefill) and the
+ * generator (decode) to minimise the modelled total time of N requests:
+ *   T_tot = ceil(N / B_pre) * T_pre(B_pre, S)
+ *         + ceil(N / B_dec) * S_dec * T_dec(B_dec, S_dec / 2)
+ * subject to B_pre * KV_v(S) + B_dec * KV_g(S_dec) <= M, with
+ * T = max(FLOPs / peak_flops, bytes / peak_bw) per batch (roofline). For a
+ * model m: a prefill of b sequences of s tokens costs 2 params b s +
+ * 2 L d b s (s + 1) flops (dense layers; causal attention) and
+ * weight_bytes + b kv s bytes (weights read once, KV written); a decode step
+ * of b sequences over c cached tokens costs 2 params b + 4 L d b c flops
+ * and weight_bytes + b kv c bytes (KV read); KV_m(s) = kv_bytes_per_token s.
+ * The search tries every prefill batch 1 <= B_pre <= N that leaves room for
+ * one decode sequence, with the decode batch on the memory boundary,
+ * B_dec = min(N, floor((M - B_pre KV_v(S)) / KV_g(S_dec))), and keeps the
+ * fastest pair, ties going to the larger B_dec. (Batches are capped at N:
+ * a batch never holds more requests than there are.) Host calls. */
+typedef struct {
+  double params;             /* parameter count */
+  double weight_bytes;       /* bytes of weights read per forward pass */
+  double kv_bytes_per_token; /* KV bytes of one token of one sequence, > 0 */
+  int32_t num_layers;        /* L */
+  int32_t attn_dim;          /* d: query heads x head size */
+} tts_model_cost;
+
+typedef struct {
+  tts_model_cost verifier, generator;
+  int64_t num_requests; /* N */
+  int64_t verify_len;   /* S: verifier input length */
+  int64_t decode_len;   /* S_dec: generated tokens per request */
+  double mem_bytes;     /* M */
+  double peak_flops;    /* P, FLOP/s */
+  double peak_bw;       /* BW, bytes/s */
+} tts_alloc_problem;
+
+typedef struct {
+  int64_t b_pre, b_dec;
+  double t_tot, t_pre, t_dec; /* seconds */
+} tts_alloc_result;
+
+/* The modelled times of one choice (b_pre, b_dec >= 1; the memory budget is
+ * not checked). */
+tts_status tts_kv_alloc_time(const tts_alloc_problem* pr, int64_t b_pre, int64_t b_dec, tts_alloc_result* out);
+
+/* The search; TTS_ERR_NOMEM when M holds no prefill and decode sequence. */
+tts_status tts_kv_alloc_search(const tts_alloc_problem* pr, tts_alloc_result* out);
+
 /* Thread-local text of the last error ("" if none). */
 const char* tts_last_error(void);
 

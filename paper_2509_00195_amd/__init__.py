@@ -16,6 +16,8 @@ from .tts import (  # noqa: F401
     tts_build_prefix_meta,
     tts_copy_blocks,
     tts_fork_tables,
+    tts_kv_alloc_search,
+    tts_kv_alloc_time,
     tts_paged_decode_attn,
     tts_paged_decode_workspace_size,
     tts_prefix_decode_attn,

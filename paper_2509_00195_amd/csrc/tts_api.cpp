@@ -20,6 +20,8 @@ hipError_t launch_merge(const MergeParams& p, int head_dim, int kv_kind, hipStre
 hipError_t launch_append(const void* k_new, const void* v_new, const int32_t* block_tables, const int32_t* seq_lens,
                          void* k_cache, void* v_cache, float* k_scale, float* v_scale, int num_seqs, int max_blocks,
                          int num_blocks, int hkv, int head_dim, int kv_kind, hipStream_t stream);
+void alloc_time(const tts_alloc_problem& pr, int64_t b_pre, int64_t b_dec, tts_alloc_result* out);
+bool alloc_search(const tts_alloc_problem& pr, tts_alloc_result* out);
 hipError_t launch_copy_blocks(const int32_t* pairs, int num_pairs, void* k_cache, void* v_cache, float* k_scale,
                               float* v_scale, int64_t blk_bytes, int num_blocks, hipStream_t stream);
 }  // namespace tts
@@ -503,6 +505,40 @@ tts_status tts_fork_tables(int32_t num_parents, const int32_t* parent_tables, in
       ++*num_copies;
     }
   }
+  return ok();
+}
+
+// ---- roofline-guided KV allocation --------------------------------------------
+
+static tts_status check_alloc(const tts_alloc_problem* pr) {
+  if (!pr) return fail(TTS_ERR_INVALID_ARG, "problem is NULL");
+  if (pr->num_requests < 1 || pr->verify_len < 1 || pr->decode_len < 1)
+    return fail(TTS_ERR_INVALID_ARG, "num_requests, verify_len and decode_len must be >= 1");
+  if (!(pr->mem_bytes > 0) || !(pr->peak_flops > 0) || !(pr->peak_bw > 0))
+    return fail(TTS_ERR_INVALID_ARG, "mem_bytes, peak_flops and peak_bw must be > 0");
+  const tts_model_cost* ms[2] = {&pr->verifier, &pr->generator};
+  for (const tts_model_cost* m : ms)
+    if (!(m->kv_bytes_per_token > 0) || !(m->params >= 0) || !(m->weight_bytes >= 0) || m->num_layers < 0 ||
+        m->attn_dim < 0)
+      return fail(TTS_ERR_INVALID_ARG, "model cost fields out of range (kv_bytes_per_token must be > 0)");
+  return TTS_OK;
+}
+
+tts_status tts_kv_alloc_time(const tts_alloc_problem* pr, int64_t b_pre, int64_t b_dec, tts_alloc_result* out) {
+  tts_status s = check_alloc(pr);
+  if (s != TTS_OK) return s;
+  if (!out) return fail(TTS_ERR_INVALID_ARG, "out is NULL");
+  if (b_pre < 1 || b_dec < 1) return fail(TTS_ERR_INVALID_ARG, "batch sizes must be >= 1");
+  tts::alloc_time(*pr, b_pre, b_dec, out);
+  return ok();
+}
+
+tts_status tts_kv_alloc_search(const tts_alloc_problem* pr, tts_alloc_result* out) {
+  tts_status s = check_alloc(pr);
+  if (s != TTS_OK) return s;
+  if (!out) return fail(TTS_ERR_INVALID_ARG, "out is NULL");
+  if (!tts::alloc_search(*pr, out))
+    return fail(TTS_ERR_NOMEM, "the budget does not hold one prefill and one decode sequence");
   return ok();
 }
 

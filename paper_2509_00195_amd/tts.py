@@ -35,7 +35,8 @@ EXPORTED = [
     "tts_build_prefix_meta", "tts_prefix_meta_destroy", "tts_prefix_meta_export", "tts_prefix_meta_coverage",
     "tts_prefix_meta_stats", "tts_paged_decode_workspace_size", "tts_paged_decode_attn",
     "tts_prefix_decode_workspace_size", "tts_prefix_decode_attn", "tts_prefix_decode_partials",
-    "tts_prefix_decode_merge", "tts_append_kv", "tts_copy_blocks", "tts_fork_tables", "tts_last_error",
+    "tts_prefix_decode_merge", "tts_append_kv", "tts_copy_blocks", "tts_fork_tables", "tts_kv_alloc_time",
+    "tts_kv_alloc_search", "tts_last_error",
 ]
 
 
@@ -49,6 +50,22 @@ class tts_attn_desc(C.Structure):
     _fields_ = [("num_q_heads", C.c_int32), ("num_kv_heads", C.c_int32), ("head_dim", C.c_int32),
                 ("block_size", C.c_int32), ("q_dtype", C.c_int), ("kv_dtype", C.c_int), ("out_dtype", C.c_int),
                 ("scale", C.c_float)]
+
+
+class tts_model_cost(C.Structure):
+    _fields_ = [("params", C.c_double), ("weight_bytes", C.c_double), ("kv_bytes_per_token", C.c_double),
+                ("num_layers", C.c_int32), ("attn_dim", C.c_int32)]
+
+
+class tts_alloc_problem(C.Structure):
+    _fields_ = [("verifier", tts_model_cost), ("generator", tts_model_cost), ("num_requests", C.c_int64),
+                ("verify_len", C.c_int64), ("decode_len", C.c_int64), ("mem_bytes", C.c_double),
+                ("peak_flops", C.c_double), ("peak_bw", C.c_double)]
+
+
+class tts_alloc_result(C.Structure):
+    _fields_ = [("b_pre", C.c_int64), ("b_dec", C.c_int64), ("t_tot", C.c_double), ("t_pre", C.c_double),
+                ("t_dec", C.c_double)]
 
 
 class tts_prefix_meta_view(C.Structure):
@@ -109,6 +126,10 @@ def load() -> C.CDLL:
     lib.tts_append_kv.argtypes = [P(tts_attn_desc), I32, VP, VP, VP, I32, VP, I32, VP, VP, VP, VP, VP]
     lib.tts_copy_blocks.restype = C.c_int
     lib.tts_copy_blocks.argtypes = [P(tts_attn_desc), I32, VP, I32, VP, VP, VP, VP, VP]
+    lib.tts_kv_alloc_time.restype = C.c_int
+    lib.tts_kv_alloc_time.argtypes = [P(tts_alloc_problem), I64, I64, P(tts_alloc_result)]
+    lib.tts_kv_alloc_search.restype = C.c_int
+    lib.tts_kv_alloc_search.argtypes = [P(tts_alloc_problem), P(tts_alloc_result)]
     lib.tts_fork_tables.restype = C.c_int
     lib.tts_fork_tables.argtypes = [I32, pi32, I32, pi32, I32, I32, pi32, pi32, pi32, I32, pi32, pi32, pi32, pi32]
     _lib = lib
@@ -309,3 +330,15 @@ def tts_fork_tables(parent_tables, parent_lens, block_size: int, child_parent, c
                                _as_i32p(cl), _as_i32p(fr), fr.shape[0], _as_i32p(ct), _as_i32p(cps),
                                C.byref(ncp), C.byref(nfu)))
     return ct[:nc, :mb], cps[: ncp.value], nfu.value
+
+
+def tts_kv_alloc_time(problem: tts_alloc_problem, b_pre: int, b_dec: int) -> tts_alloc_result:
+    r = tts_alloc_result()
+    _check(load().tts_kv_alloc_time(C.byref(problem), b_pre, b_dec, C.byref(r)))
+    return r
+
+
+def tts_kv_alloc_search(problem: tts_alloc_problem) -> tts_alloc_result:
+    r = tts_alloc_result()
+    _check(load().tts_kv_alloc_search(C.byref(problem), C.byref(r)))
+    return r
