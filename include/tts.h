@@ -330,6 +330,28 @@ tts_status tts_kv_alloc_time(const tts_alloc_problem* pr, int64_t b_pre, int64_t
 /* The search; TTS_ERR_NOMEM when M holds no prefill and decode sequence. */
 tts_status tts_kv_alloc_search(const tts_alloc_problem* pr, tts_alloc_result* out);
 
+/* ---- Dynamic prefix-aware scheduling (Sec. 4.2) ----------------------------
+ *
+ * Orders the active reasoning paths (CoTs) of a search iteration so that
+ * consecutive ones share long prefixes, and cuts the order into batches
+ * that fit a KV budget. A CoT is a path of node ids from the root (a node
+ * is a beam step; the ids of one CoT are distinct; CoT c is
+ * cot_nodes[cot_offsets[c] .. cot_offsets[c + 1])). Order: CoT 0 first,
+ * then repeatedly the remaining CoT with the longest common prefix with the
+ * last one scheduled, ties to the earliest in the input (which keeps the
+ * relative order of the parents' groups). Batches: from the front, the
+ * longest run of consecutive CoTs whose trie (the union of their nodes,
+ * each weighing node_weight[node], or 1 when node_weight is NULL) weighs at
+ * most budget; a CoT heavier than the budget is a batch of its own.
+ * Outputs (host, caller-allocated): order[num_cots]; batch_offsets
+ * [num_batches + 1] (at most num_cots + 1) into order; score = the sum of
+ * common-prefix lengths of consecutive CoTs; cost = sum over batches of
+ * trie weight minus the weight shared with the next batch (the paper's
+ * eviction cost). Host call. */
+tts_status tts_prefix_schedule(int32_t num_cots, const int32_t* cot_offsets, const int32_t* cot_nodes,
+                               int32_t num_nodes, const int64_t* node_weight, int64_t budget, int32_t* order,
+                               int32_t* batch_offsets, int32_t* num_batches, int64_t* score, int64_t* cost);
+
 /* Thread-local text of the last error ("" if none). */
 const char* tts_last_error(void);
 

@@ -18,6 +18,7 @@ from .tts import (  # noqa: F401
     tts_fork_tables,
     tts_kv_alloc_search,
     tts_kv_alloc_time,
+    tts_prefix_schedule,
     tts_paged_decode_attn,
     tts_paged_decode_workspace_size,
     tts_prefix_decode_attn,

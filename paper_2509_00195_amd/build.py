@@ -26,7 +26,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{os.path.join(ROOT, 'include')}", f"
 DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 SOURCES_HIP = ["tts_kernels.hip", "tts_kv.hip"]
-SOURCES_HOST = ["tts_meta.cpp", "tts_plan.cpp", "tts_alloc.cpp", "tts_api.cpp"]
+SOURCES_HOST = ["tts_meta.cpp", "tts_plan.cpp", "tts_alloc.cpp", "tts_sched.cpp", "tts_api.cpp"]
 
 
 def _run(cmd):

@@ -21,6 +21,18 @@ hipError_t launch_append(const void* k_new, const void* v_new, const int32_t* bl
                          void* k_cache, void* v_cache, float* k_scale, float* v_scale, int num_seqs, int max_blocks,
                          int num_blocks, int hkv, int head_dim, int kv_kind, hipStream_t stream);
 void alloc_time(const tts_alloc_problem& pr, int64_t b_pre, int64_t b_dec, tts_alloc_result* out);
+struct SchedInput {
+  int32_t num_cots;
+  const int32_t* cot_off;
+  const int32_t* cot_nodes;
+  const int64_t* weight;
+  int64_t budget;
+};
+struct SchedOutput {
+  std::vector<int32_t> order, batch_off;
+  int64_t score = 0, cost = 0;
+};
+void prefix_schedule(const SchedInput& in, SchedOutput* out);
 bool alloc_search(const tts_alloc_problem& pr, tts_alloc_result* out);
 hipError_t launch_copy_blocks(const int32_t* pairs, int num_pairs, void* k_cache, void* v_cache, float* k_scale,
                               float* v_scale, int64_t blk_bytes, int num_blocks, hipStream_t stream);
@@ -539,6 +551,39 @@ tts_status tts_kv_alloc_search(const tts_alloc_problem* pr, tts_alloc_result* ou
   if (!out) return fail(TTS_ERR_INVALID_ARG, "out is NULL");
   if (!tts::alloc_search(*pr, out))
     return fail(TTS_ERR_NOMEM, "the budget does not hold one prefill and one decode sequence");
+  return ok();
+}
+
+// ---- prefix-aware scheduling -------------------------------------------------
+
+tts_status tts_prefix_schedule(int32_t num_cots, const int32_t* cot_offsets, const int32_t* cot_nodes,
+                               int32_t num_nodes, const int64_t* node_weight, int64_t budget, int32_t* order,
+                               int32_t* batch_offsets, int32_t* num_batches, int64_t* score, int64_t* cost) {
+  if (num_cots < 0 || num_nodes < 0) return fail(TTS_ERR_INVALID_ARG, "negative size");
+  if (!num_batches || !score || !cost) return fail(TTS_ERR_INVALID_ARG, "NULL output");
+  if (num_cots > 0 && (!cot_offsets || !order || !batch_offsets)) return fail(TTS_ERR_INVALID_ARG, "NULL host array");
+  if (num_cots > 0 && cot_offsets[0] != 0) return fail(TTS_ERR_INVALID_ARG, "cot_offsets[0] must be 0");
+  for (int32_t c = 0; c < num_cots; ++c)
+    if (cot_offsets[c + 1] < cot_offsets[c]) return fail(TTS_ERR_INVALID_ARG, "cot_offsets not monotone");
+  const int32_t total = num_cots > 0 ? cot_offsets[num_cots] : 0;
+  if (total > 0 && !cot_nodes) return fail(TTS_ERR_INVALID_ARG, "NULL cot_nodes");
+  for (int32_t j = 0; j < total; ++j)
+    if (cot_nodes[j] < 0 || cot_nodes[j] >= num_nodes) return fail(TTS_ERR_OUT_OF_RANGE, "node id outside [0, num_nodes)");
+  if (node_weight)
+    for (int32_t v = 0; v < num_nodes; ++v)
+      if (node_weight[v] < 0) return fail(TTS_ERR_INVALID_ARG, "negative node weight");
+  tts::SchedInput in{num_cots, cot_offsets, cot_nodes, node_weight, budget};
+  tts::SchedOutput out;
+  try {
+    tts::prefix_schedule(in, &out);
+  } catch (const std::bad_alloc&) {
+    return fail(TTS_ERR_NOMEM, "host allocation failed");
+  }
+  std::copy(out.order.begin(), out.order.end(), order);
+  if (num_cots > 0) std::copy(out.batch_off.begin(), out.batch_off.end(), batch_offsets);
+  *num_batches = num_cots > 0 ? static_cast<int32_t>(out.batch_off.size()) - 1 : 0;
+  *score = out.score;
+  *cost = out.cost;
   return ok();
 }
 

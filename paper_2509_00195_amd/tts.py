@@ -36,7 +36,7 @@ EXPORTED = [
     "tts_prefix_meta_stats", "tts_paged_decode_workspace_size", "tts_paged_decode_attn",
     "tts_prefix_decode_workspace_size", "tts_prefix_decode_attn", "tts_prefix_decode_partials",
     "tts_prefix_decode_merge", "tts_append_kv", "tts_copy_blocks", "tts_fork_tables", "tts_kv_alloc_time",
-    "tts_kv_alloc_search", "tts_last_error",
+    "tts_kv_alloc_search", "tts_prefix_schedule", "tts_last_error",
 ]
 
 
@@ -130,6 +130,8 @@ def load() -> C.CDLL:
     lib.tts_kv_alloc_time.argtypes = [P(tts_alloc_problem), I64, I64, P(tts_alloc_result)]
     lib.tts_kv_alloc_search.restype = C.c_int
     lib.tts_kv_alloc_search.argtypes = [P(tts_alloc_problem), P(tts_alloc_result)]
+    lib.tts_prefix_schedule.restype = C.c_int
+    lib.tts_prefix_schedule.argtypes = [I32, pi32, pi32, I32, P(C.c_int64), I64, pi32, pi32, pi32, P(I64), P(I64)]
     lib.tts_fork_tables.restype = C.c_int
     lib.tts_fork_tables.argtypes = [I32, pi32, I32, pi32, I32, I32, pi32, pi32, pi32, I32, pi32, pi32, pi32, pi32]
     _lib = lib
@@ -342,3 +344,25 @@ def tts_kv_alloc_search(problem: tts_alloc_problem) -> tts_alloc_result:
     r = tts_alloc_result()
     _check(load().tts_kv_alloc_search(C.byref(problem), C.byref(r)))
     return r
+
+
+def tts_prefix_schedule(cots, num_nodes: int, budget: int, node_weight=None):
+    """Host call. cots: list of node-id paths. Returns (order, batch list of order slices, score, cost)."""
+    lib = load()
+    lens = [len(c) for c in cots]
+    offs = _host_i32(np.concatenate([[0], np.cumsum(lens)]) if cots else [0])
+    nodes = _host_i32(np.concatenate([np.asarray(c, np.int32) for c in cots]) if sum(lens) else np.zeros(0))
+    n = len(cots)
+    order = np.zeros(max(n, 1), np.int32)
+    boff = np.zeros(n + 1, np.int32)
+    nb, sc, co = C.c_int32(0), C.c_int64(0), C.c_int64(0)
+    wp = None
+    if node_weight is not None:
+        w = np.ascontiguousarray(np.asarray(node_weight, np.int64))
+        wp = w.ctypes.data_as(C.POINTER(C.c_int64))
+    _check(lib.tts_prefix_schedule(n, _as_i32p(offs), _as_i32p(nodes) if nodes.size else None, num_nodes, wp,
+                                   int(budget), _as_i32p(order), _as_i32p(boff), C.byref(nb), C.byref(sc),
+                                   C.byref(co)))
+    order = order[:n]
+    batches = [order[boff[i]:boff[i + 1]].tolist() for i in range(nb.value)]
+    return order, batches, sc.value, co.value
