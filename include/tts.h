@@ -205,6 +205,34 @@ tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta*
                                   const int32_t* seq_lens, int32_t num_blocks, void* out, void* workspace,
                                   size_t workspace_bytes, hipStream_t stream);
 
+/* ---- Verification attention over the shared prefix (LookAhead
+ * Verification, Sec. 4.1: the current and the speculative step go to the
+ * verifier as one request; its attention is a multi-token causal attention
+ * over each path's shared prefix). Every beam's last q_len cached tokens are
+ * queries: query i of beam b (position seq_lens[b] - q_len + i) attends to
+ * the beam's tokens 0 .. seq_lens[b] - q_len + i (causal). The metadata
+ * (tts_build_verify_meta) treats query i of beam b as a virtual beam
+ * b * q_len + i whose length ends at that position, so the shared blocks are
+ * read once for every query row of every beam that shares them.
+ * tts_build_verify_meta: as tts_build_prefix_meta, plus q_len >= 1; every
+ * seq_len must be >= q_len. Exported views and coverage rows describe the
+ * virtual beams. */
+tts_status tts_build_verify_meta(int32_t num_reqs, const int32_t* req_seq_offsets, int32_t num_seqs,
+                                 const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                                 int32_t q_len, int32_t block_size, int32_t num_blocks, const tts_attn_desc* desc,
+                                 hipStream_t stream, tts_prefix_meta** out);
+
+/* q: [num_seqs][q_len][Hq][D], out: [num_seqs][q_len][Hq][D] fp32;
+ * block_tables [num_seqs][max_blocks_per_seq] and seq_lens [num_seqs] are
+ * the beams' own (device); the other arguments and rules are those of
+ * tts_prefix_decode_attn (which refuses a verification metadata). The
+ * partials/merge pair below also accepts a verification metadata. */
+tts_status tts_prefix_verify_attn(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
+                                  const void* k_cache, const void* v_cache, const float* k_scale,
+                                  const float* v_scale, const int32_t* block_tables, int32_t max_blocks_per_seq,
+                                  const int32_t* seq_lens, int32_t num_blocks, void* out, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream);
+
 /* The two launches of tts_prefix_decode_attn, for callers that schedule
  * them separately (to overlap the merge with other work, or to time the
  * attention kernel alone). tts_prefix_decode_partials runs the work units

@@ -6,7 +6,9 @@ slow and written to be checked by eye against its definitions:
 * ``attention.oracle_attn`` -- single-query softmax attention per beam and
   query head over the beam's fully materialised key/value sequence, read
   through its block table (the paged KV cache of the paper's serving
-  substrate, Sec. 2.3), in fp32.
+  substrate, Sec. 2.3), in fp32; ``attention.oracle_verify_attn`` -- the
+  same with each beam's last q_len tokens as causal queries (the verifier
+  pass over the current and speculative steps, Sec. 4.1).
 * ``prefix_meta.oracle_prefix_meta`` -- the beams of each request arranged
   as a radix tree (trie) of shared full-block prefixes, grouped so that beams
   spawned from the same parent are adjacent while the parents keep their
@@ -28,7 +30,7 @@ No part of this oracle is "parity unpinned": every function is checked in
 routine or hand-derived golden fixtures.
 """
 
-from .attention import decode_bf16, oracle_attn, oracle_attn_row  # noqa: F401
+from .attention import decode_bf16, oracle_attn, oracle_attn_row, oracle_verify_attn  # noqa: F401
 from .fp8 import e4m3_table  # noqa: F401
 from .kv_ops import append_kv, copy_blocks, e4m3_encode, fork_tables  # noqa: F401
 from .prefix_meta import oracle_coverage, oracle_prefix_meta  # noqa: F401

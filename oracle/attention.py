@@ -143,3 +143,48 @@ def oracle_attn_workload(wl, scale=None, beams=None) -> np.ndarray:
         num_q_heads=sh.num_q_heads, num_kv_heads=sh.num_kv_heads, block_size=sh.block_size,
         q_dtype=sh.q_dtype, kv_dtype=sh.kv_dtype, scale=scale, beams=beams,
     )
+
+
+def oracle_verify_attn(
+    q: np.ndarray,
+    k_cache: np.ndarray,
+    v_cache: np.ndarray,
+    k_scale: Optional[np.ndarray],
+    v_scale: Optional[np.ndarray],
+    block_tables: np.ndarray,
+    seq_lens: np.ndarray,
+    q_len: int,
+    *,
+    num_q_heads: int,
+    num_kv_heads: int,
+    block_size: int,
+    q_dtype: str,
+    kv_dtype: str,
+    scale: Optional[float] = None,
+    beams=None,
+) -> np.ndarray:
+    """Verification attention (LookAhead Verification, Sec. 4.1: a verifier pass over a path's
+    current and speculative steps at once): each beam's last ``q_len`` cached tokens are
+    queries, query i at position p_i = L - q_len + i attending causally to tokens 0 .. p_i.
+
+    q: [S, q_len, Hq, D]; returns float32 [S, q_len, Hq, D]."""
+    s_all = seq_lens.shape[0]
+    d = q.shape[-1]
+    g = num_q_heads // num_kv_heads
+    sc = np.float32(1.0 / math.sqrt(d) if scale is None or scale <= 0 else scale)
+    out = np.zeros((s_all, q_len, num_q_heads, d), dtype=np.float32)
+    for b in (range(s_all) if beams is None else beams):
+        length = int(seq_lens[b])
+        assert length >= q_len
+        nblk = -(-length // block_size)
+        ids = np.asarray(block_tables[b, :nblk], dtype=np.int64)
+        k_seq, v_seq = _beam_kv(k_cache, v_cache, k_scale, v_scale, ids, length, kv_dtype)
+        qb = _decode(q[b], q_dtype)  # [q_len, Hq, D]
+        for i in range(q_len):
+            visible = length - q_len + i + 1  # tokens 0 .. p_i
+            for h in range(num_q_heads):
+                kvh = h // g
+                s = (k_seq[kvh, :visible] @ qb[i, h]).astype(np.float32) * sc
+                p = np.exp(s - s.max())
+                out[b, i, h] = (p @ v_seq[kvh, :visible]) / p.sum(dtype=np.float32)
+    return out

@@ -14,11 +14,13 @@ from .tts import (  # noqa: F401
     make_desc,
     tts_append_kv,
     tts_build_prefix_meta,
+    tts_build_verify_meta,
     tts_copy_blocks,
     tts_fork_tables,
     tts_kv_alloc_search,
     tts_kv_alloc_time,
     tts_prefix_schedule,
+    tts_prefix_verify_attn,
     tts_paged_decode_attn,
     tts_paged_decode_workspace_size,
     tts_prefix_decode_attn,

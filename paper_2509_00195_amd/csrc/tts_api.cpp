@@ -103,6 +103,7 @@ struct tts_prefix_meta {
   tts_attn_desc desc{};
   tts::WorkPlan plan;
   int32_t num_blocks = 0;
+  int32_t q_len = 1;  // > 1: a verification metadata (q_len virtual beams per beam)
   // device buffer: unit records | slot table | build_len
   void* dev = nullptr;
   size_t off_recs = 0, off_slot_tab = 0, off_build = 0;
@@ -112,10 +113,10 @@ extern "C" {
 
 const char* tts_last_error(void) { return g_last_error.c_str(); }
 
-tts_status tts_build_prefix_meta(int32_t num_reqs, const int32_t* req_seq_offsets, int32_t num_seqs,
-                                 const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
-                                 int32_t block_size, int32_t num_blocks, const tts_attn_desc* desc,
-                                 hipStream_t stream, tts_prefix_meta** out) {
+static tts_status build_meta_impl(int32_t num_reqs, const int32_t* req_seq_offsets, int32_t num_seqs,
+                                  const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                                  int32_t block_size, int32_t num_blocks, const tts_attn_desc* desc,
+                                  hipStream_t stream, int32_t q_len, tts_prefix_meta** out) {
   if (!out) return fail(TTS_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   if (desc) {
@@ -147,6 +148,7 @@ tts_status tts_build_prefix_meta(int32_t num_reqs, const int32_t* req_seq_offset
     return fail(static_cast<tts_status>(rc), err);
   }
   m->num_blocks = num_blocks;
+  m->q_len = q_len;
   if (desc) {
     m->has_plan = true;
     m->desc = *desc;
@@ -190,6 +192,42 @@ tts_status tts_build_prefix_meta(int32_t num_reqs, const int32_t* req_seq_offset
   }
   *out = m;
   return ok();
+}
+
+tts_status tts_build_prefix_meta(int32_t num_reqs, const int32_t* req_seq_offsets, int32_t num_seqs,
+                                 const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                                 int32_t block_size, int32_t num_blocks, const tts_attn_desc* desc,
+                                 hipStream_t stream, tts_prefix_meta** out) {
+  return build_meta_impl(num_reqs, req_seq_offsets, num_seqs, block_tables, max_blocks_per_seq, seq_lens, block_size,
+                         num_blocks, desc, stream, 1, out);
+}
+
+tts_status tts_build_verify_meta(int32_t num_reqs, const int32_t* req_seq_offsets, int32_t num_seqs,
+                                 const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                                 int32_t q_len, int32_t block_size, int32_t num_blocks, const tts_attn_desc* desc,
+                                 hipStream_t stream, tts_prefix_meta** out) {
+  if (!out) return fail(TTS_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (q_len < 1) return fail(TTS_ERR_INVALID_ARG, "q_len must be >= 1");
+  if (num_reqs < 0 || num_seqs < 0 || max_blocks_per_seq < 0) return fail(TTS_ERR_INVALID_ARG, "negative size");
+  if ((num_seqs > 0 && (!seq_lens || !block_tables)) || !req_seq_offsets)
+    return fail(TTS_ERR_INVALID_ARG, "NULL host array");
+  const int64_t vs = static_cast<int64_t>(num_seqs) * q_len;
+  if (vs > 0x7FFFFFFF / 2) return fail(TTS_ERR_UNSUPPORTED, "too many query rows");
+  for (int32_t b = 0; b < num_seqs; ++b)
+    if (seq_lens[b] < q_len) return fail(TTS_ERR_INVALID_ARG, "a beam is shorter than q_len");
+  // Virtual beams b * q_len + i: beam b's table, its first len - (q_len - 1 - i) tokens.
+  std::vector<int32_t> voff(num_reqs + 1), vlen(vs), vtab(static_cast<size_t>(vs) * max_blocks_per_seq);
+  for (int32_t r = 0; r <= num_reqs; ++r) voff[r] = req_seq_offsets[r] * q_len;
+  for (int32_t b = 0; b < num_seqs; ++b)
+    for (int32_t i = 0; i < q_len; ++i) {
+      const int64_t v = static_cast<int64_t>(b) * q_len + i;
+      vlen[v] = seq_lens[b] - (q_len - 1 - i);
+      std::memcpy(vtab.data() + v * max_blocks_per_seq, block_tables + static_cast<int64_t>(b) * max_blocks_per_seq,
+                  sizeof(int32_t) * max_blocks_per_seq);
+    }
+  return build_meta_impl(num_reqs, voff.data(), static_cast<int32_t>(vs), vtab.data(), max_blocks_per_seq,
+                         vlen.data(), block_size, num_blocks, desc, stream, q_len, out);
 }
 
 void tts_prefix_meta_destroy(tts_prefix_meta* m) {
@@ -296,6 +334,7 @@ tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const
   p.scale_log2 = scale_log2(d);
   p.paged_nsplit = ns;
   p.paged_max_len = max_seq_len;
+  p.q_len = 1;
   const int64_t units = static_cast<int64_t>(num_seqs) * d->num_kv_heads * ns;
   if (units > 0x7FFFFFFF) return fail(TTS_ERR_UNSUPPORTED, "grid too large");
   hipError_t e = tts::launch_attn(p, static_cast<int>(units), d->head_dim, kv_kind(d), stream);
@@ -374,6 +413,7 @@ tts_status prefix_params(const tts_attn_desc* d, const tts_prefix_meta* m, const
   p->hkv = d->num_kv_heads;
   p->g = d->num_q_heads / d->num_kv_heads;
   p->scale_log2 = scale_log2(d);
+  p->q_len = m->q_len;
   return TTS_OK;
 }
 
@@ -398,6 +438,7 @@ tts_status launch_prefix_merge(const tts_attn_desc* d, const tts_prefix_meta* m,
   mp.num_seqs = p.num_seqs;
   mp.hq = d->num_q_heads;
   mp.g = p.g;
+  mp.q_len = p.q_len;
   mp.rows_per_head = p.rows_per_head;
   hipError_t e = tts::launch_merge(mp, d->head_dim, kv_kind(d), stream);
   if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("merge launch: ") + hipGetErrorString(e));
@@ -407,6 +448,22 @@ tts_status launch_prefix_merge(const tts_attn_desc* d, const tts_prefix_meta* m,
 }  // namespace
 
 tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
+                                  const void* k_cache, const void* v_cache, const float* k_scale,
+                                  const float* v_scale, const int32_t* block_tables, int32_t max_blocks_per_seq,
+                                  const int32_t* seq_lens, int32_t num_blocks, void* out, void* workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  if (m && m->q_len != 1)
+    return fail(TTS_ERR_INVALID_ARG, "verification metadata (q_len > 1): use tts_prefix_verify_attn");
+  tts::AttnParams p;
+  tts_status s = prefix_params(d, m, q, k_cache, v_cache, k_scale, v_scale, block_tables, max_blocks_per_seq,
+                               seq_lens, num_blocks, out, workspace, workspace_bytes, true, &p);
+  if (s != TTS_OK || m->host.num_seqs == 0) return s == TTS_OK ? ok() : s;
+  if ((s = launch_partials(d, m, p, stream)) != TTS_OK) return s;
+  if ((s = launch_prefix_merge(d, m, p, stream)) != TTS_OK) return s;
+  return ok();
+}
+
+tts_status tts_prefix_verify_attn(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
                                   const void* k_cache, const void* v_cache, const float* k_scale,
                                   const float* v_scale, const int32_t* block_tables, int32_t max_blocks_per_seq,
                                   const int32_t* seq_lens, int32_t num_blocks, void* out, void* workspace,

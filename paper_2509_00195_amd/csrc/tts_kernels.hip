@@ -641,6 +641,14 @@ __device__ __forceinline__ UnitRegs load_unit(const UnitRec* recs, int idx, int 
 
 // Live and build-time lengths of the beams whose entries depend on them
 // (the partial last block, the extension marker), loaded by those lanes.
+// Current length of beam vb: for verification, virtual beam b * q_len + i
+// is beam b's first seq_lens[b] - (q_len - 1 - i) tokens.
+template <typename P>
+__device__ __forceinline__ int beam_len(const P& p, int vb) {
+  if (p.q_len <= 1) return p.seq_lens[vb];
+  return p.seq_lens[vb / p.q_len] - (p.q_len - 1 - vb % p.q_len);
+}
+
 __device__ __forceinline__ void issue_live(const AttnParams& p, const UnitRegs& u, int lane, int* len, int* build) {
   const bool live = lane < u.nent && (u.ent_inf & (kEntLive | kEntExt)) != 0;
   const int slot = (u.ent_inf & kEntExt) ? u.ent_id : static_cast<int>(ent_r0(u.ent_inf)) / p.g;
@@ -648,7 +656,7 @@ __device__ __forceinline__ void issue_live(const AttnParams& p, const UnitRegs& 
   *len = 0;
   *build = 0;
   if (live) {
-    *len = p.seq_lens[lb];
+    *len = beam_len(p, lb);
     *build = p.build_len[lb];
   }
 }
@@ -1026,7 +1034,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
         bool xbad = false;
         if (lane < cn) {
           const int j = xnext + lane;
-          id = p.block_tables[static_cast<int64_t>(xb) * p.max_blocks + j];
+          id = p.block_tables[static_cast<int64_t>(xb / p.q_len) * p.max_blocks + j];
           v = xlen - j * kTok;
           v = v < kTok ? v : kTok;
           if (id < 0 || id >= p.num_blocks) {
@@ -1194,7 +1202,7 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
     for (int k = 0; k < kBatch; ++k) ent[k] = 0;
     head_base = 0;
   }
-  const int L = p.seq_lens[b];
+  const int L = beam_len(p, b);
   bool nan = p.build_len && L < p.build_len[b];
   float mx = kNegInf, den = 0.f;
   f32x2 acc = {0.f, 0.f};

@@ -98,6 +98,11 @@ struct AttnParams {
   float scale_log2;      // softmax scale * log2(e)
   int32_t paged_nsplit;  // paged path: splits per beam (1: write the output directly)
   int32_t paged_max_len;
+  // Verification: every beam's last q_len tokens are queries, each a
+  // virtual beam vb = b * q_len + i over beam b's table with length
+  // seq_lens[b] - (q_len - 1 - i) (causal). 1 for decode.
+  int32_t q_len;
+  int32_t pad2;
 };
 
 // Slots the merge kernel reads per round trip (and the smallest slot-table
@@ -120,7 +125,7 @@ struct MergeParams {
   int32_t g;
   int32_t rows_per_head;
   int32_t paged_nsplit;
-  int32_t pad;
+  int32_t q_len;  // as in AttnParams (lengths of virtual beams)
 };
 
 }  // namespace tts

@@ -36,7 +36,8 @@ EXPORTED = [
     "tts_prefix_meta_stats", "tts_paged_decode_workspace_size", "tts_paged_decode_attn",
     "tts_prefix_decode_workspace_size", "tts_prefix_decode_attn", "tts_prefix_decode_partials",
     "tts_prefix_decode_merge", "tts_append_kv", "tts_copy_blocks", "tts_fork_tables", "tts_kv_alloc_time",
-    "tts_kv_alloc_search", "tts_prefix_schedule", "tts_last_error",
+    "tts_kv_alloc_search", "tts_prefix_schedule", "tts_build_verify_meta", "tts_prefix_verify_attn",
+    "tts_last_error",
 ]
 
 
@@ -100,6 +101,9 @@ def load() -> C.CDLL:
     lib.tts_last_error.argtypes = []
     lib.tts_build_prefix_meta.restype = C.c_int
     lib.tts_build_prefix_meta.argtypes = [I32, pi32, I32, pi32, I32, pi32, I32, I32, P(tts_attn_desc), VP, P(VP)]
+    lib.tts_build_verify_meta.restype = C.c_int
+    lib.tts_build_verify_meta.argtypes = [I32, pi32, I32, pi32, I32, pi32, I32, I32, I32, P(tts_attn_desc), VP,
+                                          P(VP)]
     lib.tts_prefix_meta_destroy.restype = None
     lib.tts_prefix_meta_destroy.argtypes = [VP]
     lib.tts_prefix_meta_export.restype = C.c_int
@@ -118,6 +122,8 @@ def load() -> C.CDLL:
     lib.tts_prefix_decode_attn.restype = C.c_int
     lib.tts_prefix_decode_attn.argtypes = [P(tts_attn_desc), VP, VP, VP, VP, VP, VP, VP, I32, VP, I32, VP, VP,
                                            C.c_size_t, VP]
+    lib.tts_prefix_verify_attn.restype = C.c_int
+    lib.tts_prefix_verify_attn.argtypes = lib.tts_prefix_decode_attn.argtypes
     lib.tts_prefix_decode_partials.restype = C.c_int
     lib.tts_prefix_decode_partials.argtypes = lib.tts_prefix_decode_attn.argtypes
     lib.tts_prefix_decode_merge.restype = C.c_int
@@ -221,6 +227,21 @@ def tts_build_prefix_meta(req_seq_offsets, block_tables, seq_lens, block_size: i
     h = C.c_void_p()
     _check(lib.tts_build_prefix_meta(offs.shape[0] - 1, _as_i32p(offs), s, _as_i32p(tables), maxb, _as_i32p(lens),
                                      block_size, num_blocks, C.byref(desc) if desc is not None else None,
+                                     _stream(stream) if desc is not None else None, C.byref(h)))
+    return PrefixMeta(h.value, desc)
+
+
+def tts_build_verify_meta(req_seq_offsets, block_tables, seq_lens, q_len: int, block_size: int, num_blocks: int,
+                          desc: Optional[tts_attn_desc] = None, stream=None) -> PrefixMeta:
+    lib = load()
+    offs = _host_i32(req_seq_offsets)
+    tables = _host_i32(block_tables)
+    lens = _host_i32(seq_lens)
+    s = lens.shape[0]
+    maxb = tables.shape[1] if tables.ndim == 2 else 0
+    h = C.c_void_p()
+    _check(lib.tts_build_verify_meta(offs.shape[0] - 1, _as_i32p(offs), s, _as_i32p(tables), maxb, _as_i32p(lens),
+                                     q_len, block_size, num_blocks, C.byref(desc) if desc is not None else None,
                                      _stream(stream) if desc is not None else None, C.byref(h)))
     return PrefixMeta(h.value, desc)
 
@@ -366,3 +387,12 @@ def tts_prefix_schedule(cots, num_nodes: int, budget: int, node_weight=None):
     order = order[:n]
     batches = [order[boff[i]:boff[i + 1]].tolist() for i in range(nb.value)]
     return order, batches, sc.value, co.value
+
+
+def tts_prefix_verify_attn(desc: tts_attn_desc, meta: PrefixMeta, q, k_cache, v_cache, k_scale, v_scale,
+                           block_tables, max_blocks_per_seq: int, seq_lens, num_blocks: int, out, workspace,
+                           workspace_bytes: int, stream=None):
+    _check(load().tts_prefix_verify_attn(
+        C.byref(desc), meta.handle, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_scale), _ptr(v_scale),
+        _ptr(block_tables), max_blocks_per_seq, _ptr(seq_lens), num_blocks, _ptr(out), _ptr(workspace),
+        workspace_bytes, _stream(stream)))

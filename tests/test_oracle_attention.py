@@ -267,3 +267,62 @@ def test_e4m3_to_bf16_is_exact():
     fin = np.isfinite(t)
     back = torch.from_numpy(t[fin]).to(torch.bfloat16).float().numpy()
     assert np.array_equal(back, t[fin])
+
+
+# ---- verification attention (each beam's last q_len tokens as causal queries) ----
+
+def run_verify(q, kc, vc, tables, lens, q_len, hq, hkv, q_dtype="f32", kv_dtype="f32"):
+    from oracle import oracle_verify_attn
+
+    return oracle_verify_attn(q, kc, vc, None, None, tables, lens, q_len, num_q_heads=hq, num_kv_heads=hkv,
+                              block_size=BS, q_dtype=q_dtype, kv_dtype=kv_dtype)
+
+
+@pytest.mark.parametrize("q_len", [1, 3, 16])
+def test_verify_matches_masked_sdpa_f64(q_len):
+    """Against torch SDPA in float64 with an explicit mask: query i of a beam of length L sees
+    keys 0 .. L - q_len + i."""
+    rng = np.random.default_rng(40 + q_len)
+    hq, hkv, d = 12, 2, 64
+    lens = [q_len, q_len + 5, 40, 16 + q_len]
+    ks, vs = rand_dense(rng, lens, hkv, d)
+    q = rng.standard_normal((len(lens), q_len, hq, d)).astype(np.float32)
+    kc, vc, tables, L = scatter_paged(ks, vs, BS, rng)
+    got = run_verify(q, kc, vc, tables, L, q_len, hq, hkv)
+    for b, ln in enumerate(lens):
+        mask = np.arange(ln)[None, :] <= (ln - q_len + np.arange(q_len))[:, None]  # [q_len, L]
+        qt = torch.from_numpy(q[b].transpose(1, 0, 2).astype(np.float64))  # [Hq, q_len, D]
+        kt = torch.from_numpy(np.repeat(ks[b], hq // hkv, axis=0).astype(np.float64))
+        vt = torch.from_numpy(np.repeat(vs[b], hq // hkv, axis=0).astype(np.float64))
+        ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, attn_mask=torch.from_numpy(mask))
+        assert np.max(np.abs(got[b] - ref.numpy().transpose(1, 0, 2))) < 1e-5
+
+
+def test_verify_with_one_query_is_decode():
+    rng = np.random.default_rng(50)
+    hq, hkv, d = 8, 2, 32
+    lens = [1, 17, 33]
+    ks, vs = rand_dense(rng, lens, hkv, d)
+    q = rng.standard_normal((len(lens), hq, d)).astype(np.float32)
+    kc, vc, tables, L = scatter_paged(ks, vs, BS, rng)
+    assert np.array_equal(run_verify(q[:, None], kc, vc, tables, L, 1, hq, hkv)[:, 0],
+                          run_oracle(q, kc, vc, tables, L, hq, hkv))
+
+
+def test_verify_is_causal():
+    """Changing a key/value after query i's position leaves query i unchanged; at it, changes it."""
+    rng = np.random.default_rng(51)
+    hq, hkv, d, q_len = 4, 1, 32, 4
+    lens = [21]
+    ks, vs = rand_dense(rng, lens, hkv, d)
+    q = rng.standard_normal((1, q_len, hq, d)).astype(np.float32)
+    kc, vc, tables, L = scatter_paged(ks, vs, BS, rng)
+    base = run_verify(q, kc, vc, tables, L, q_len, hq, hkv)
+    pos = 21 - q_len + 1  # position of query 1
+    blk, slot = tables[0, pos // BS], pos % BS
+    kc2, vc2 = kc.copy(), vc.copy()
+    kc2[blk, :, slot, :] += 3.0
+    vc2[blk, :, :, slot] -= 2.0
+    moved = run_verify(q, kc2, vc2, tables, L, q_len, hq, hkv)
+    assert np.array_equal(moved[0, 0], base[0, 0])  # query 0 ends before that position
+    assert np.max(np.abs(moved[0, 1] - base[0, 1])) > 1e-3  # query 1 sees it
