@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--layers", type=int, default=28)
     ap.add_argument("--variant", choices=["prefix", "paged"], default="prefix")
     ap.add_argument("--graph", action="store_true", help="replay the steps from a captured HIP graph")
+    ap.add_argument("--q-len", type=int, default=1,
+                    help="verification: every beam's last Q tokens are causal queries (prefix variant only; "
+                         "value is then query tokens/s)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--check", action="store_true", help="compare layer 0 against the oracle")
@@ -206,12 +209,29 @@ def main():
 
     pools = make_layers(wl, x, args.layers, args.seed)
     out = pref.out
+    qlen = max(1, args.q_len)
+    if qlen > 1:
+        if args.variant != "prefix":
+            raise SystemExit("--q-len needs the prefix variant")
+        vmeta = T.tts_build_verify_meta(wl.req_seq_offsets, wl.block_tables, wl.seq_lens, qlen, 16, wl.num_blocks,
+                                        desc=pref.desc, stream=stream)
+        vws_bytes = T.tts_prefix_decode_workspace_size(pref.desc, vmeta)
+        vws = torch.zeros(max(vws_bytes, 1), dtype=torch.uint8, device=dev)
+        out = torch.zeros((wl.num_seqs, qlen, sh.num_q_heads, sh.head_dim), dtype=torch.float32, device=dev)
+        gq = torch.Generator(device=dev)
+        gq.manual_seed(2000 + args.seed)
+        qv = torch.randn((wl.num_seqs, qlen, sh.num_q_heads, sh.head_dim), generator=gq, device=dev)
+        qv = qv if sh.q_dtype == "f32" else qv.to(torch.bfloat16)
+        units, slots = vmeta.stats()
     tabs, lens = x.block_tables, x.seq_lens
     maxb = int(tabs.shape[1])
 
     def step(i, partials_only=False):
         q, k, v, ks, vs = pools[i % len(pools)]
-        if args.variant == "prefix":
+        if qlen > 1:
+            fn = T.tts_prefix_decode_partials if partials_only else T.tts_prefix_verify_attn
+            fn(pref.desc, vmeta, qv, k, v, ks, vs, tabs, maxb, lens, wl.num_blocks, out, vws, vws_bytes, stream)
+        elif args.variant == "prefix":
             fn = T.tts_prefix_decode_partials if partials_only else T.tts_prefix_decode_attn
             fn(pref.desc, pref.meta, q, k, v, ks, vs, tabs, maxb, lens, wl.num_blocks, out, pref.ws, pref.ws_bytes,
                stream)
@@ -220,7 +240,7 @@ def main():
                                     wl.num_blocks, out, paged.ws, paged.ws_bytes, stream)
 
     check = None
-    if args.check:
+    if args.check and qlen == 1:
         from oracle.attention import oracle_attn_workload
 
         step(0)
@@ -260,7 +280,7 @@ def main():
         ms = timed(lambda n: [step(i) for i in range(n)], args.steps)
         steps = args.steps
     ms_per_step = ms / steps
-    value = wl.num_seqs / (ms_per_step * 1e-3)
+    value = wl.num_seqs * qlen / (ms_per_step * 1e-3)
 
     # The dominant kernel alone (the attention work units of each call), same
     # rotation, events on the stream it runs on.
@@ -322,7 +342,7 @@ def main():
     rec = {
         "metric": METRIC,
         "value": value,
-        "unit": "beam-tokens/s",
+        "unit": "beam-tokens/s" if qlen == 1 else "query-tokens/s",
         "n_gpus": 1,
         "steps": steps,
         "warmup": args.warmup,
@@ -340,6 +360,7 @@ def main():
             "beams": wl.num_seqs,
             "layers_rotated": len(pools),
             "graph_replay": bool(args.graph),
+            "q_len": qlen,
             "unique_kv_bytes": int(unique_kv),
             "logical_kv_bytes": int(logical_kv),
             "sharing": logical_kv / max(unique_kv, 1),
