@@ -819,11 +819,23 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
         unsigned char* stages = lds + Q::bytes;
         const int np = (nst + 1) >> 1;
         const int tpw = (nt + kWaves - 1) / kWaves;
-        auto pair_ids = [&](int pp, int* id0, int* id1) {
+        // Entries (e0, e1) and block ids of pair pp.
+        int e0, e1, id0, id1;
+        auto pair_ids = [&](int pp) {
           pp = pp < np ? pp : np - 1;  // past the end: a repeat of the last pair (a cache hit, never used)
-          *id0 = rl(u.ent_id, 2 * pp);
-          *id1 = 2 * pp + 1 < nst ? rl(u.ent_id, 2 * pp + 1) : *id0;
+          e0 = 2 * pp;
+          e1 = 2 * pp + 1 < nst ? 2 * pp + 1 : e0;
+          id0 = rl(u.ent_id, e0);
+          id1 = rl(u.ent_id, e1);
         };
+        // fp8: lane i holds the K and V scales of entry i, read once per unit.
+        float ksl = 1.f, vsl = 1.f;
+        if constexpr (KV == kKvFp8) {
+          if (lane < nst) {
+            ksl = p.k_scale[u.ent_id];
+            vsl = p.v_scale[u.ent_id];
+          }
+        }
         RowState<D> st[kWideTiles];
         float m_exact[kWideTiles];
 #pragma unroll
@@ -838,24 +850,22 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             st[i].seen = kNegInf;
           }
           Quarter<D, KV> qa, qb;
-          // fp8: the pair's block scales (K of block 0, 1; V of block 0, 1),
-          // loaded with its quarter.
+          // fp8: the pair's block scales (K of block 0, 1; V of block 0, 1).
           f32x4 sa, sb;
-          auto scales = [&](int i0, int i1) {
+          auto scales = [&]() {
             if constexpr (KV == kKvFp8)
-              return f32x4{p.k_scale[i0], p.k_scale[i1], p.v_scale[i0], p.v_scale[i1]};
+              return f32x4{rlf(ksl, e0), rlf(ksl, e1), rlf(vsl, e0), rlf(vsl, e1)};
             else
               return f32x4{1.f, 1.f, 1.f, 1.f};
           };
-          int id0, id1;
-          pair_ids(0, &id0, &id1);
+          pair_ids(0);
           load_quarter<D, KV>(qa, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
-          sa = scales(id0, id1);
+          sa = scales();
           __syncthreads();  // every wave is done with the stage area (previous unit or attempt)
           auto step = [&](Quarter<D, KV>& cur, Quarter<D, KV>& nxt, const f32x4& cs, f32x4& ns, int pp) {
-            pair_ids(pp + 1, &id0, &id1);
+            pair_ids(pp + 1);
             load_quarter<D, KV>(nxt, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
-            ns = scales(id0, id1);
+            ns = scales();
             unsigned char* stage = stages + (pp & 1) * SG::bytes;
             store_quarter<D, KV>(cur, stage, wave, lane);
             __syncthreads();  // the whole pair is in the stage
