@@ -89,13 +89,12 @@ struct Geo {
 
 __device__ __forceinline__ uint32_t f32_bits(float x) { return __builtin_bit_cast(uint32_t, x); }
 
-// Two OCP E4M3 codes (byte pair kHi of w) -> two bf16 in one dword. The
-// conversion to fp32 is exact and every E4M3 value fits bf16 exactly, so
-// dropping the low half of the fp32 pattern is exact too.
+// Two OCP E4M3 codes (byte pair kHi of w) -> two bf16 in one dword, in one
+// conversion instruction with unit scale. Every E4M3 value fits bf16
+// exactly, so the conversion is exact.
 template <bool kHi>
 __device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t w) {
-  f32x2 f = __builtin_amdgcn_cvt_pk_f32_fp8(w, kHi);
-  return (f32_bits(f.x) >> 16) | (f32_bits(f.y) & 0xFFFF0000u);
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, kHi));
 }
 
 __device__ __forceinline__ uint4 fp8x8_to_bf16x8(uint2 w) {
