@@ -312,6 +312,7 @@ tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const
   if (need > 0 && (!workspace || workspace_bytes < need))
     return fail(TTS_ERR_WORKSPACE, "workspace smaller than tts_paged_decode_workspace_size");
   const size_t rows = static_cast<size_t>(num_seqs) * ns * d->num_q_heads;
+  if (rows > 0x7FFFFFFFu) return fail(TTS_ERR_UNSUPPORTED, "more than 2^31 - 1 partial rows");
   tts::AttnParams p{};
   p.q = q;
   p.k_cache = k_cache;
@@ -391,6 +392,7 @@ tts_status prefix_params(const tts_attn_desc* d, const tts_prefix_meta* m, const
   if (!workspace || workspace_bytes < need)
     return fail(TTS_ERR_WORKSPACE, "workspace smaller than tts_prefix_decode_workspace_size");
   const size_t rows = static_cast<size_t>(m->plan.rows_per_head) * d->num_kv_heads;
+  if (rows > 0x7FFFFFFFu) return fail(TTS_ERR_UNSUPPORTED, "more than 2^31 - 1 partial rows");
   const char* dev = static_cast<const char*>(m->dev);
   *p = tts::AttnParams{};
   p->q = q;

@@ -1175,17 +1175,68 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
   }
 }
 
+// kEpl consecutive stored elements of a partial row (fp16 or fp32), loaded
+// with one or two vector loads and widened one at a time.
+template <int kEpl, bool F16>
+struct MergeRaw;
+template <>
+struct MergeRaw<8, true> {
+  typedef uint4 T;
+  static __device__ __forceinline__ T load(const void* base, int64_t off) {
+    return *reinterpret_cast<const uint4*>(static_cast<const _Float16*>(base) + off);
+  }
+  static __device__ __forceinline__ float get(const T& t, int i) {
+    const uint32_t w = i < 2 ? t.x : (i < 4 ? t.y : (i < 6 ? t.z : t.w));
+    const f16x2 hv = __builtin_bit_cast(f16x2, w);
+    return static_cast<float>((i & 1) ? hv.y : hv.x);
+  }
+};
+template <>
+struct MergeRaw<4, true> {
+  typedef uint2 T;
+  static __device__ __forceinline__ T load(const void* base, int64_t off) {
+    return *reinterpret_cast<const uint2*>(static_cast<const _Float16*>(base) + off);
+  }
+  static __device__ __forceinline__ float get(const T& t, int i) {
+    const f16x2 hv = __builtin_bit_cast(f16x2, i < 2 ? t.x : t.y);
+    return static_cast<float>((i & 1) ? hv.y : hv.x);
+  }
+};
+template <>
+struct MergeRaw<8, false> {
+  struct T {
+    f32x4 a, b;
+  };
+  static __device__ __forceinline__ T load(const void* base, int64_t off) {
+    const f32x4* src = reinterpret_cast<const f32x4*>(static_cast<const float*>(base) + off);
+    return T{src[0], src[1]};
+  }
+  static __device__ __forceinline__ float get(const T& t, int i) { return i < 4 ? t.a[i] : t.b[i - 4]; }
+};
+template <>
+struct MergeRaw<4, false> {
+  typedef f32x4 T;
+  static __device__ __forceinline__ T load(const void* base, int64_t off) {
+    return *reinterpret_cast<const f32x4*>(static_cast<const float*>(base) + off);
+  }
+  static __device__ __forceinline__ float get(const T& t, int i) { return t[i]; }
+};
+
 // Exact merge of the partial softmax states of each (beam, query head), in
 // the order of the beam's slot list. With M = max_k m_k and
 // w_k = l_k 2^(m_k - M), and e_k the stored elements o_k / (l_k s_k):
 //   out = sum_k w_k s_k e_k / sum_k w_k.
-// One wave per row (2 output dims per lane). A row's slot count and first
-// kMergeBatch slots sit in one row of the slot table and are loaded together
-// with the beam's lengths; then the states of kMergeBatch slots at a time,
-// so a row costs two round trips to memory (more only past kMergeBatch
-// slots).
+// Two kernels compute it; launch_merge picks by the number of rows.
+//
+// merge_row_kernel: D / 2 lanes per row (2 elements per lane), for batches
+// with few rows, where spreading each row over many lanes shortens the
+// work after the data arrives. A row's slot count and first kMergeBatch
+// slots sit in one row of the slot table and are loaded with the beam's
+// lengths; then kMergeBatch states at a time, the table entries of the
+// next batch loaded with them: 1 + ceil(n / kMergeBatch) round trips to
+// memory for n slots.
 template <int D, bool F16>
-__global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
+__global__ __launch_bounds__(kThreads) void merge_row_kernel(MergeParams p) {
   constexpr int kTpr = D / 2;
   constexpr int kRows = kThreads / kTpr;
   constexpr int kBatch = kMergeBatch;
@@ -1216,10 +1267,6 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
   float mx = kNegInf, den = 0.f;
   f32x2 acc = {0.f, 0.f};
   for (int k0 = 0; k0 < n; k0 += kBatch) {
-    if (k0 > 0 && tab) {
-#pragma unroll
-      for (int k = 0; k < kBatch; ++k) ent[k] = k0 + k < n ? tab[1 + k0 + k] : 0;
-    }
     f32x4 ml[kBatch];
     f32x2 o[kBatch];
 #pragma unroll
@@ -1237,6 +1284,12 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
       } else {
         o[k] = *reinterpret_cast<const f32x2*>(static_cast<const float*>(p.part_o) + row * D + pos0);
       }
+    }
+    // The next batch's table entries travel with this batch's states
+    // (stride >= n + 1, so the reads stay inside the beam's table row).
+    if (tab && k0 + kBatch < n) {
+#pragma unroll
+      for (int k = 0; k < kBatch; ++k) ent[k] = k0 + kBatch + k < n ? tab[1 + k0 + kBatch + k] : 0;
     }
 #pragma unroll
     for (int k = 0; k < kBatch; ++k)
@@ -1269,6 +1322,122 @@ __global__ __launch_bounds__(kThreads) void merge_kernel(MergeParams p) {
   *reinterpret_cast<f32x2*>(p.out + static_cast<int64_t>(r) * D + d0) = w;
 }
 
+// merge_kernel: for batches with many rows. One wave per workgroup, sixteen
+// lanes per row, each lane holding D / 16 consecutive stored elements (one
+// or two 16-byte loads per state). Lane j of a row holds slot table entries
+// j, j + 16, ... (the first kMergeTabChunks
+// chunks are read in the first round trip to memory, with the beam's
+// lengths); for a batch of 16 slots, lane j reads slot j's (m, l, s) and
+// every lane reads its elements of every slot of the batch, the slots' rows
+// shuffled across the row's lanes: one round trip per batch. The weights
+// are added in slot order.
+constexpr int kMergeLanes = 16;
+// Up to this many rows the one-row-per-wave kernel runs (about the waves
+// the GPU keeps resident at its occupancy); above, the sixteen-lane one.
+constexpr int kMergeRowKernelMaxRows = 4096;
+constexpr int kMergeTabChunks = 4;
+constexpr int kMergeThreads = 64;
+template <int D, bool F16>
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p) {
+  constexpr int kLpr = kMergeLanes;
+  constexpr int kEpl = D / kLpr;              // stored elements per lane
+  constexpr int kRows = kMergeThreads / kLpr;  // rows per workgroup
+  constexpr int kBatch = kLpr;                // slots whose states are loaded together
+  const int lane = threadIdx.x & 63;
+  const int j = lane & (kLpr - 1);
+  const int gbase = lane & ~(kLpr - 1);  // first lane of this row's group
+  const int total = p.num_seqs * p.hq;
+  const int r_raw = static_cast<int>(blockIdx.x) * kRows + static_cast<int>(threadIdx.x) / kLpr;
+  const bool valid = r_raw < total;
+  const int r = valid ? r_raw : total - 1;  // surplus rows repeat the last one and store nothing
+  const int b = r / p.hq;
+  const int h = r % p.hq;
+  const int* tab = p.slot_tab ? p.slot_tab + static_cast<int64_t>(b) * p.slot_stride : nullptr;
+  const int n = tab ? tab[0] : p.paged_nsplit;
+  const int head_base = tab ? (h / p.g) * p.rows_per_head + h % p.g : 0;
+  // Partial row of slot k (k < n).
+  auto slot_row = [&](int k, int entry) { return tab ? head_base + entry : (b * p.paged_nsplit + k) * p.hq + h; };
+  int ent[kMergeTabChunks];
+#pragma unroll
+  for (int c = 0; c < kMergeTabChunks; ++c) {
+    const int k = kBatch * c + j;
+    ent[c] = (tab && k < n) ? tab[1 + k] : 0;
+  }
+  const int L = beam_len(p, b);
+  bool nan = p.build_len && L < p.build_len[b];
+  float mx = kNegInf, den = 0.f;
+  float acc[kEpl];
+#pragma unroll
+  for (int e = 0; e < kEpl; ++e) acc[e] = 0.f;
+  for (int k0 = 0, c = 0; k0 < n; k0 += kBatch, ++c) {
+    // Lane j: slot k0 + j (a repeat of slot k0 past the end).
+    const bool has = k0 + j < n;
+    const int kk = has ? k0 + j : k0;
+    int entry = 0;
+    if (tab) {
+      if (c < kMergeTabChunks) {
+        entry = ent[0];
+#pragma unroll
+        for (int i = 1; i < kMergeTabChunks; ++i)
+          if (c == i) entry = ent[i];
+        const int first = __shfl(entry, gbase);  // slot k0's entry (every lane takes part)
+        if (!has) entry = first;
+      } else {
+        entry = tab[1 + kk];
+      }
+    }
+    const int row_j = slot_row(kk, entry);
+    f32x4 ml = *reinterpret_cast<const f32x4*>(p.part_ml + static_cast<int64_t>(row_j) * kPartMl);
+    typename MergeRaw<kEpl, F16>::T raw[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int row_k = __shfl(row_j, gbase + k);
+      raw[k] = MergeRaw<kEpl, F16>::load(p.part_o, static_cast<int64_t>(row_k) * D + kEpl * j);
+    }
+    if (!has) ml = f32x4{kNegInf, 0.f, 0.f, 0.f};
+    nan |= ml.x != ml.x;
+    float bm = ml.x;
+#pragma unroll
+    for (int o = 1; o < kLpr; o <<= 1) bm = fmaxf(bm, __shfl_xor(bm, o));
+    const float mn = fmaxf(mx, bm);
+    if (mn == kNegInf) continue;  // uniform over the row's lanes
+    const float a = (mx == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(mx - mn);
+    den *= a;
+#pragma unroll
+    for (int i = 0; i < kEpl; ++i) acc[i] *= a;
+    const float w = (ml.x == kNegInf) ? 0.f : ml.y * __builtin_amdgcn_exp2f(ml.x - mn);
+    const float ws = w * ml.z;
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const float wk = __shfl(w, gbase + k);
+      const float wsk = __shfl(ws, gbase + k);
+      if (k0 + k < n) {
+        den += wk;
+#pragma unroll
+        for (int i = 0; i < kEpl; ++i) acc[i] += MergeRaw<kEpl, F16>::get(raw[k], i) * wsk;
+      }
+    }
+    mx = mn;
+  }
+  // A NaN state in any slot of the row makes the row NaN.
+  int any_nan = nan ? 1 : 0;
+#pragma unroll
+  for (int o = 1; o < kLpr; o <<= 1) any_nan |= __shfl_xor(any_nan, o);
+  if (!valid) return;
+  const float inv = (den > 0.f && L > 0) ? 1.f / den : 0.f;
+  const float q = __builtin_nanf("");
+  float* orow = p.out + static_cast<int64_t>(r) * D;
+  // Stored position pos holds dimension 16 t + 4 lq + i for pos = (D/4) lq + 4 t + i.
+#pragma unroll
+  for (int c = 0; c < kEpl / 4; ++c) {
+    const int pos = kEpl * j + 4 * c;
+    const int dim = 16 * ((pos % (D / 4)) / 4) + 4 * (pos / (D / 4));
+    f32x4 v = {acc[4 * c] * inv, acc[4 * c + 1] * inv, acc[4 * c + 2] * inv, acc[4 * c + 3] * inv};
+    if (any_nan) v = f32x4{q, q, q, q};
+    *reinterpret_cast<f32x4*>(orow + dim) = v;
+  }
+}
+
 template <int D, int KV>
 static hipError_t launch_attn_t(const AttnParams& p, int grid, hipStream_t stream) {
   hipLaunchKernelGGL((attn_kernel<D, KV>), dim3(grid), dim3(kThreads), 0, stream, p);
@@ -1278,19 +1447,35 @@ static hipError_t launch_attn_t(const AttnParams& p, int grid, hipStream_t strea
 hipError_t launch_merge(const MergeParams& p, int head_dim, int kv_kind, hipStream_t stream) {
   const int rows = p.num_seqs * p.hq;
   if (rows <= 0) return hipSuccess;
-  const int per = kThreads / (head_dim / 2);
-  const int blocks = (rows + per - 1) / per;
   const bool f16 = kv_kind != kKvF32;
+  if (rows <= kMergeRowKernelMaxRows) {
+    const int per = kThreads / (head_dim / 2);
+    const int blocks = (rows + per - 1) / per;
+    if (head_dim == 128) {
+      if (f16)
+        hipLaunchKernelGGL((merge_row_kernel<128, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+      else
+        hipLaunchKernelGGL((merge_row_kernel<128, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+    } else {
+      if (f16)
+        hipLaunchKernelGGL((merge_row_kernel<64, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+      else
+        hipLaunchKernelGGL((merge_row_kernel<64, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+    }
+    return hipGetLastError();
+  }
+  const int per = kMergeThreads / kMergeLanes;  // rows per workgroup
+  const int blocks = (rows + per - 1) / per;
   if (head_dim == 128) {
     if (f16)
-      hipLaunchKernelGGL((merge_kernel<128, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+      hipLaunchKernelGGL((merge_kernel<128, true>), dim3(blocks), dim3(kMergeThreads), 0, stream, p);
     else
-      hipLaunchKernelGGL((merge_kernel<128, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+      hipLaunchKernelGGL((merge_kernel<128, false>), dim3(blocks), dim3(kMergeThreads), 0, stream, p);
   } else {
     if (f16)
-      hipLaunchKernelGGL((merge_kernel<64, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+      hipLaunchKernelGGL((merge_kernel<64, true>), dim3(blocks), dim3(kMergeThreads), 0, stream, p);
     else
-      hipLaunchKernelGGL((merge_kernel<64, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+      hipLaunchKernelGGL((merge_kernel<64, false>), dim3(blocks), dim3(kMergeThreads), 0, stream, p);
   }
   return hipGetLastError();
 }

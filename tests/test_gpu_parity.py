@@ -204,6 +204,26 @@ def test_head_dim_64_bf16():
     assert err(op, ref) <= TOL["bf16"] and err(ox, ref) <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("kv,head_dim", [("f32", 64), ("f32", 128), ("bf16", 64), ("fp8", 128)])
+def test_many_rows_merge(kv, head_dim):
+    """More than 4096 (beam, query head) rows: the merge runs its many-row
+    kernel (sixteen lanes per row); sequences past 1024 tokens give the paged
+    path split partials too."""
+    from tts_synth import ReqSpec, WorkloadConfig
+
+    shape = AttnShape(16, 4, head_dim, 16, "f32" if kv == "f32" else "bf16", kv)
+    spec = ReqSpec(beams=40, branch=4, prompt=(512, 512), step=(64, 256), max_len=1400)
+    cfg = WorkloadConfig("many_rows", shape, (spec,) * 8)
+    wl = make_workload(cfg, 5)
+    assert len(wl.seq_lens) * shape.num_q_heads > 4096 and wl.max_seq_len > 1024
+    ref = oracle_attn_workload(wl)
+    op, ox = outputs(wl)
+    tol = TOL[kv]
+    print(f"many rows {kv} D{head_dim}: paged {err(op, ref):.2e} prefix {err(ox, ref):.2e}", flush=True)
+    assert np.isfinite(op).all() and np.isfinite(ox).all()
+    assert err(op, ref) <= tol and err(ox, ref) <= tol
+
+
 def test_scale_override():
     wl = make_workload("tiny", 1)
     x = to_device(wl)
