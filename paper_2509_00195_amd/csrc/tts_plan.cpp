@@ -51,6 +51,10 @@ constexpr double kRowUs = 0.08;  // per row of 256 + 272 bytes (query + partial 
 constexpr double kWideUsPerByte = 0.193 / 8192;
 constexpr double kTileBlockUs = 0.113;  // per block and row tile of a wave, D = 128
 constexpr int kXcds = 8;  // workgroup k of a launch runs on XCD k % 8
+// The merge (a second launch): a fixed cost plus one round trip to memory
+// per kMergeBatch partial states of the beam with the most.
+constexpr double kMergeFixedUs = 3.2;
+constexpr double kMergeBatchUs = 1.4;
 
 int tiles_of(int rows) { return (rows + 15) / 16; }
 
@@ -91,6 +95,18 @@ struct Work {
   int32_t t, kvh;
   double cost;
 };
+
+// Which of a unit's beams (t.lo + i) it writes partial states for: all of
+// a wide unit's; a narrow unit's whose rows some entry covers.
+void touched_beams(const Tmpl& t, int32_t g, std::vector<char>* out) {
+  const int32_t nb = t.hi - t.lo;
+  out->assign(nb, t.mode == kModeWide ? 1 : 0);
+  for (size_t k = 0; t.mode == kModeNarrow && k < t.ids.size(); ++k) {
+    const uint32_t inf = t.info[k];
+    const int32_t r0 = inf & 63, r1 = ((inf >> 6) & 63) + 1;
+    for (int32_t i = r0 / g; i < (r1 + g - 1) / g && i < nb; ++i) (*out)[i] = 1;
+  }
+}
 
 }  // namespace
 
@@ -393,7 +409,34 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
       else
         lo = mid;
     }
-    units_at(hi);
+    // Longer units mean fewer partial states per beam, so a cheaper merge:
+    // take the target (the smallest one's variable part scaled up) with the
+    // least modelled attention plus merge time.
+    std::vector<char> touched;
+    auto most_slots = [&](const std::vector<Tmpl>& t) {
+      std::vector<int32_t> cnt(S, 0);
+      for (const Tmpl& x : t) {
+        touched_beams(x, g, &touched);
+        for (int32_t i = 0; i < x.hi - x.lo; ++i)
+          if (touched[i]) ++cnt[m.perm[x.lo + i]];
+      }
+      return S > 0 ? *std::max_element(cnt.begin(), cnt.end()) : 0;
+    };
+    const double t_min = hi;
+    double best_T = t_min, best_est = -1;
+    for (double f : {1.0, 1.5, 2.0, 3.0, 4.0, 6.0}) {
+      const double T = kUnitFixedUs + f * (t_min - kUnitFixedUs);
+      if (units_at(T) > fit_units) continue;
+      double ms = 0;
+      for (const Tmpl& x : tm) ms = std::max(ms, x.cost);
+      const int32_t slots = most_slots(tm);
+      const double est = ms + kMergeFixedUs + kMergeBatchUs * ((slots + kMergeBatch - 1) / kMergeBatch);
+      if (best_est < 0 || est < best_est) {
+        best_est = est;
+        best_T = T;
+      }
+    }
+    units_at(best_T);
     place(tm, ngroups, bins);
   } else {
     std::vector<Tmpl> cand;
@@ -419,12 +462,8 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
   for (size_t t = 0; t < tm.size(); ++t) {
     prow0[t] = rows;
     const int32_t nb = tm[t].hi - tm[t].lo;
-    std::vector<char> touched(nb, tm[t].mode == kModeWide ? 1 : 0);
-    for (size_t k = 0; tm[t].mode == kModeNarrow && k < tm[t].ids.size(); ++k) {
-      const uint32_t inf = tm[t].info[k];
-      const int32_t r0 = inf & 63, r1 = ((inf >> 6) & 63) + 1;
-      for (int32_t i = r0 / g; i < (r1 + g - 1) / g && i < nb; ++i) touched[i] = 1;
-    }
+    std::vector<char> touched;
+    touched_beams(tm[t], g, &touched);
     for (int32_t i = 0; i < nb; ++i)
       if (touched[i]) per_beam[m.perm[tm[t].lo + i]].push_back(rows + i * g);
     rows += nb * g;
