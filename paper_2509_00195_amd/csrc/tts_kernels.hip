@@ -848,9 +848,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             st[i].l = 0.f;
             st[i].seen = kNegInf;
           }
+          // Two quarters. bf16: each step first sends the next pair's loads
+          // into the other quarter. fp8 (quarters of half the size): each
+          // quarter is refilled with the pair two ahead as soon as it is
+          // staged, so its loads are in flight for about two steps (faster
+          // for fp8, slower for bf16 as compiled, where the wait counts of
+          // alternate steps cover both quarters).
+          constexpr bool kRefill = KV == kKvFp8;
           Quarter<D, KV> qa, qb;
           // fp8: the pair's block scales (K of block 0, 1; V of block 0, 1).
-          f32x4 sa, sb;
           auto scales = [&]() {
             if constexpr (KV == kKvFp8)
               return f32x4{rlf(ksl, e0), rlf(ksl, e1), rlf(vsl, e0), rlf(vsl, e1)};
@@ -859,14 +865,24 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
           };
           pair_ids(0);
           load_quarter<D, KV>(qa, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
-          sa = scales();
+          if constexpr (kRefill) {
+            pair_ids(1);
+            load_quarter<D, KV>(qb, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
+          }
           __syncthreads();  // every wave is done with the stage area (previous unit or attempt)
-          auto step = [&](Quarter<D, KV>& cur, Quarter<D, KV>& nxt, const f32x4& cs, f32x4& ns, int pp) {
-            pair_ids(pp + 1);
-            load_quarter<D, KV>(nxt, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
-            ns = scales();
+          auto step = [&](Quarter<D, KV>& cur, Quarter<D, KV>& nxt, int pp) {
             unsigned char* stage = stages + (pp & 1) * SG::bytes;
-            store_quarter<D, KV>(cur, stage, wave, lane);
+            if constexpr (kRefill) {
+              store_quarter<D, KV>(cur, stage, wave, lane);
+              pair_ids(pp + 2);
+              load_quarter<D, KV>(cur, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
+            } else {
+              pair_ids(pp + 1);
+              load_quarter<D, KV>(nxt, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
+              store_quarter<D, KV>(cur, stage, wave, lane);
+            }
+            pair_ids(pp);
+            const f32x4 cs = scales();
             __syncthreads();  // the whole pair is in the stage
             Ops<D, KV> o;
             read_stage<D, KV>(o, stage, lane);
@@ -893,9 +909,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             }
           };
           for (int pp = 0; pp < np; pp += 2) {
-            step(qa, qb, sa, sb, pp);
+            step(qa, qb, pp);
             if (pp + 1 >= np) break;
-            step(qb, qa, sb, sa, pp + 1);
+            step(qb, qa, pp + 1);
           }
           if (attempt == 0) TTS_PROF_MARK(1, rec_idx);
           if (attempt > 0) break;
