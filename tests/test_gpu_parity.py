@@ -204,18 +204,22 @@ def test_head_dim_64_bf16():
     assert err(op, ref) <= TOL["bf16"] and err(ox, ref) <= TOL["bf16"]
 
 
-@pytest.mark.parametrize("kv,head_dim", [("f32", 64), ("f32", 128), ("bf16", 64), ("fp8", 128)])
-def test_many_rows_merge(kv, head_dim):
-    """More than 4096 (beam, query head) rows: the merge runs its many-row
-    kernel (sixteen lanes per row); sequences past 1024 tokens give the paged
-    path split partials too."""
+def _many_rows_workload(kv, head_dim):
+    """320 beams x 16 query heads: more than 4096 (beam, query head) rows, so
+    the merge runs its many-row kernel (sixteen lanes per row); sequences past
+    1024 tokens give the paged path split partials too."""
     from tts_synth import ReqSpec, WorkloadConfig
 
     shape = AttnShape(16, 4, head_dim, 16, "f32" if kv == "f32" else "bf16", kv)
     spec = ReqSpec(beams=40, branch=4, prompt=(512, 512), step=(64, 256), max_len=1400)
-    cfg = WorkloadConfig("many_rows", shape, (spec,) * 8)
-    wl = make_workload(cfg, 5)
+    wl = make_workload(WorkloadConfig("many_rows", shape, (spec,) * 8), 5)
     assert len(wl.seq_lens) * shape.num_q_heads > 4096 and wl.max_seq_len > 1024
+    return wl
+
+
+@pytest.mark.parametrize("kv,head_dim", [("f32", 64), ("f32", 128), ("bf16", 64), ("fp8", 128)])
+def test_many_rows_merge(kv, head_dim):
+    wl = _many_rows_workload(kv, head_dim)
     ref = oracle_attn_workload(wl)
     op, ox = outputs(wl)
     tol = TOL[kv]
@@ -243,13 +247,17 @@ def test_private_appends_after_build():
     assert err(ox, ref) <= TOL["bf16"]
 
 
-def test_bad_block_id_gives_nan_row_only():
+@pytest.mark.parametrize("many_rows", [False, True])
+def test_bad_block_id_gives_nan_row_only(many_rows):
     """A block id outside the pool makes only that beam's row NaN: in the paged path for any table
     entry, in the prefix path for a block appended after the metadata was built (entries in use at
-    build time are validated by tts_build_prefix_meta)."""
-    wl = make_workload("1p5b16", 0)
+    build time are validated by tts_build_prefix_meta). Both merge kernels carry the NaN."""
+    wl = _many_rows_workload("bf16", 128) if many_rows else make_workload("1p5b16", 0)
     m = oracle_prefix_meta(wl.req_seq_offsets, wl.block_tables, wl.seq_lens, 16)
     b = 3
+    if many_rows:  # a long beam (split partials in the paged path) with a tail of two or more blocks
+        b = next(i for i in range(wl.num_seqs)
+                 if wl.seq_lens[i] > 1024 and (int(wl.seq_lens[i]) + 15) // 16 - 1 > m["tail_lblock"][i])
     last = (int(wl.seq_lens[b]) + 15) // 16 - 1
     assert last > m["tail_lblock"][b]  # a tail block that is not the first one
     short = wl.seq_lens.copy()
