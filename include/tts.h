@@ -175,7 +175,9 @@ size_t tts_paged_decode_workspace_size(const tts_attn_desc* d, int32_t num_seqs,
  * num_blocks: size of the block pool (ids outside it give NaN rows).
  * workspace: device buffer of at least tts_paged_decode_workspace_size
  * bytes (TTS_ERR_WORKSPACE otherwise); NULL allowed when that size is 0.
- * Calls that overlap in time must not share a workspace. */
+ * Calls that overlap in time must not share a workspace. More than
+ * 2^31 - 1 partial rows (num_seqs x splits x query heads) is
+ * TTS_ERR_UNSUPPORTED. */
 tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const void* q, const void* k_cache,
                                  const void* v_cache, const float* k_scale, const float* v_scale,
                                  const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
@@ -198,7 +200,8 @@ size_t tts_prefix_decode_workspace_size(const tts_attn_desc* d, const tts_prefix
  * the metadata; blocks appended since are read from block_tables.
  * block_tables/seq_lens: device copies of the current tables and lengths.
  * workspace: at least tts_prefix_decode_workspace_size bytes (partial
- * softmax states; calls that overlap in time must not share one). */
+ * softmax states; calls that overlap in time must not share one). A plan
+ * with more than 2^31 - 1 partial rows is TTS_ERR_UNSUPPORTED. */
 tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
                                   const void* k_cache, const void* v_cache, const float* k_scale,
                                   const float* v_scale, const int32_t* block_tables, int32_t max_blocks_per_seq,
