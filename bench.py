@@ -282,6 +282,20 @@ def main():
     ms_per_step = ms / steps
     value = wl.num_seqs * qlen / (ms_per_step * 1e-3)
 
+    # For reference: the same calls replayed from one captured HIP graph per
+    # rotation of the layer pools (what a serving loop that captures its
+    # decode step would see); `value` stays the eager rate.
+    graph_call_us = ms_per_step * 1e3 if graph is not None else None
+    if graph is None:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for i in range(len(pools)):
+                step(i)
+        g.replay()
+        reps = max(1, args.steps // len(pools))
+        graph_call_us = timed(lambda n: [g.replay() for _ in range(n)], reps) * 1e3 / (reps * len(pools))
+        del g
+
     # The dominant kernel alone (the attention work units of each call), same
     # rotation, events on the stream it runs on.
     if args.variant == "prefix":
@@ -360,6 +374,7 @@ def main():
             "beams": wl.num_seqs,
             "layers_rotated": len(pools),
             "graph_replay": bool(args.graph),
+            "graph_call_us": graph_call_us,
             "q_len": qlen,
             "unique_kv_bytes": int(unique_kv),
             "logical_kv_bytes": int(logical_kv),

@@ -34,7 +34,7 @@ class PagedAttention:
         dev = inputs.q.device
         self.out = torch.empty((s, inputs.shape.num_q_heads, inputs.shape.head_dim), dtype=torch.float32, device=dev)
         self.ws_bytes = _t.tts_paged_decode_workspace_size(self.desc, s, self.max_seq_len)
-        self.ws = torch.zeros(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)  # counters start at zero
+        self.ws = torch.zeros(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)  # partial softmax states
 
     def __call__(self, k_cache=None, v_cache=None, k_scale=None, v_scale=None, out=None, stream=None):
         x = self.x
@@ -62,7 +62,7 @@ class PrefixAttention:
         dev = inputs.q.device
         self.out = torch.empty((s, inputs.shape.num_q_heads, inputs.shape.head_dim), dtype=torch.float32, device=dev)
         self.ws_bytes = _t.tts_prefix_decode_workspace_size(self.desc, self.meta)
-        self.ws = torch.zeros(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)  # counters start at zero
+        self.ws = torch.zeros(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)  # partial softmax states
 
     def __call__(self, k_cache=None, v_cache=None, k_scale=None, v_scale=None, out=None,
                  seq_lens: Optional[torch.Tensor] = None, stream=None):
