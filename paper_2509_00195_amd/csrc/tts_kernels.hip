@@ -818,21 +818,30 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
         unsigned char* stages = lds + Q::bytes;
         const int np = (nst + 1) >> 1;
         const int tpw = (nt + kWaves - 1) / kWaves;
-        // Entries (e0, e1) and block ids of pair pp.
+        // A wide unit has up to kMaxWideEntries blocks: entry i < 64 in lane
+        // i of ent_id, entry 64 + i in lane i of the info words (which wide
+        // units do not need). Entries (e0, e1) and block ids of pair pp; a
+        // pair never straddles the two halves.
         int e0, e1, id0, id1;
         auto pair_ids = [&](int pp) {
           pp = pp < np ? pp : np - 1;  // past the end: a repeat of the last pair (a cache hit, never used)
           e0 = 2 * pp;
           e1 = 2 * pp + 1 < nst ? 2 * pp + 1 : e0;
-          id0 = rl(u.ent_id, e0);
-          id1 = rl(u.ent_id, e1);
+          const int ids = e0 < kMaxEntries ? u.ent_id : static_cast<int>(u.ent_inf);
+          id0 = rl(ids, e0 & (kMaxEntries - 1));
+          id1 = rl(ids, e1 & (kMaxEntries - 1));
         };
-        // fp8: lane i holds the K and V scales of entry i, read once per unit.
-        float ksl = 1.f, vsl = 1.f;
+        // fp8: lane i holds the K and V scales of entries i and 64 + i, read
+        // once per unit.
+        float ksl = 1.f, vsl = 1.f, ksl2 = 1.f, vsl2 = 1.f;
         if constexpr (KV == kKvFp8) {
           if (lane < nst) {
             ksl = p.k_scale[u.ent_id];
             vsl = p.v_scale[u.ent_id];
+          }
+          if (lane + kMaxEntries < nst) {
+            ksl2 = p.k_scale[static_cast<int>(u.ent_inf)];
+            vsl2 = p.v_scale[static_cast<int>(u.ent_inf)];
           }
         }
         RowState<D> st[kWideTiles];
@@ -858,10 +867,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
           Quarter<D, KV> qa, qb;
           // fp8: the pair's block scales (K of block 0, 1; V of block 0, 1).
           auto scales = [&]() {
-            if constexpr (KV == kKvFp8)
-              return f32x4{rlf(ksl, e0), rlf(ksl, e1), rlf(vsl, e0), rlf(vsl, e1)};
-            else
+            if constexpr (KV == kKvFp8) {
+              const float ks = e0 < kMaxEntries ? ksl : ksl2, vs = e0 < kMaxEntries ? vsl : vsl2;
+              const int i0 = e0 & (kMaxEntries - 1), i1 = e1 & (kMaxEntries - 1);
+              return f32x4{rlf(ks, i0), rlf(ks, i1), rlf(vs, i0), rlf(vs, i1)};
+            } else {
               return f32x4{1.f, 1.f, 1.f, 1.f};
+            }
           };
           pair_ids(0);
           load_quarter<D, KV>(qa, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);

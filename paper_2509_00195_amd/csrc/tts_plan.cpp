@@ -224,7 +224,8 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
         const int32_t cap = mode == kModeWide ? RW : RB;
         for (int32_t C = (G + cap - 1) / cap; C <= std::min(G, 4 * ((G + cap - 1) / cap)); ++C) {
           const int32_t rows = ((G + C - 1) / C) * g;
-          for (int32_t P = std::max(1, (n + kMaxEntries - 1) / kMaxEntries); P <= np; ++P) {
+          const int32_t max_ent = mode == kModeWide ? kMaxWideEntries : kMaxEntries;
+          for (int32_t P = std::max(1, (n + max_ent - 1) / max_ent); P <= np; ++P) {
             const int32_t blocks = std::min(n, 2 * ((np + P - 1) / P));
             const double us = mode == kModeWide ? cm.wide_us(blocks, rows) : cm.narrow_us(blocks, rows);
             const double bytes = static_cast<double>(C) * P * cm.bytes(blocks, rows);
@@ -497,8 +498,12 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
     r.mode = t.mode;
     for (int32_t i = 0; i < t.hi - t.lo; ++i) r.beams[i] = m.perm[t.lo + i];
     for (size_t k = 0; k < t.ids.size(); ++k) {
-      r.ent_id[k] = t.ids[k];
-      r.ent_info[k] = t.info[k];
+      if (k < static_cast<size_t>(kMaxEntries)) {
+        r.ent_id[k] = t.ids[k];
+        r.ent_info[k] = t.info[k];
+      } else {  // wide units only: the second half of the block ids
+        r.ent_info[k - kMaxEntries] = static_cast<uint32_t>(t.ids[k]);
+      }
     }
     return r;
   };

@@ -12,12 +12,15 @@ namespace tts {
 constexpr int kMaxRows = 64;
 // Block entries per unit (one per lane of a wave).
 constexpr int kMaxEntries = 64;
+// Wide units hold up to two per lane: entry 64 + i sits in ent_info[i].
+constexpr int kMaxWideEntries = 2 * kMaxEntries;
 // Beams per unit.
 constexpr int kMaxUnitBeams = 16;
 
 // Entry info word: rows [r0, r1) of the unit that attend to the block, and
 // its valid token count (static; see the flags). Wide units' blocks apply
-// to all of their rows and are full; their info words are not read.
+// to all of their rows and are full: they need no info words, and their
+// ent_info array holds the block ids of entries 64 .. 127 instead.
 //   bits  0..5   r0
 //   bits  6..11  r1 - 1
 //   bits 12..15  valid - 1
@@ -50,7 +53,7 @@ enum UnitMode : int32_t { kModeNarrow = 0, kModeWide = 1 };
 struct UnitRec {
   int32_t kvh;
   int32_t nrows;    // 0: nothing to do (an idle workgroup)
-  int32_t nstatic;  // block entries (pairs are entries 2i, 2i+1)
+  int32_t nstatic;  // block entries (pairs are entries 2i, 2i+1); wide: up to kMaxWideEntries
   int32_t nent;     // block entries + extension entries (these come last)
   int32_t prow0;
   int32_t next;     // next record of the same workgroup, -1 at the end

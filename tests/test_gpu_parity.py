@@ -81,18 +81,24 @@ def test_parity_balanced_tree():
     assert err(op, ref) <= TOL["bf16"] and err(ox, ref) <= TOL["bf16"]
 
 
-def test_parity_longchain_fp8_sampled():
-    wl = make_workload("7b_longchain_fp8", 0)
+@pytest.mark.parametrize("kv", ["fp8", "bf16"])
+def test_parity_longchain_sampled(kv):
+    """The long-chain batch at full size (its wide units hold up to 128 blocks,
+    ids 64.. in the info words), in fp8 as configured and in bf16."""
+    cfg = CONFIGS["7b_longchain_fp8"]
+    if kv != "fp8":
+        cfg = dataclasses.replace(cfg, shape=dataclasses.replace(cfg.shape, kv_dtype=kv))
+    wl = make_workload(cfg, 0)
     s = wl.num_seqs
     rng = np.random.default_rng(0)
     rows = sorted(set(rng.choice(s, 20, replace=False).tolist()) | {int(np.argmax(wl.seq_lens)), 0, s - 1})
     ref = oracle_attn_workload(wl, beams=rows)
     op, ox = outputs(wl)
-    print(f"longchain fp8 ({len(rows)} beams): paged {err(op, ref, rows):.2e} prefix {err(ox, ref, rows):.2e}",
+    print(f"longchain {kv} ({len(rows)} beams): paged {err(op, ref, rows):.2e} prefix {err(ox, ref, rows):.2e}",
           flush=True)
     assert np.isfinite(op).all() and np.isfinite(ox).all()
-    assert err(op, ref, rows) <= TOL["fp8"] and err(ox, ref, rows) <= TOL["fp8"]
-    assert err(op, ox) <= TOL["fp8"]  # every beam: the two paths agree
+    assert err(op, ref, rows) <= TOL[kv] and err(ox, ref, rows) <= TOL[kv]
+    assert err(op, ox) <= TOL[kv]  # every beam: the two paths agree
 
 
 def test_run_to_run_deterministic():
