@@ -336,6 +336,7 @@ tts_status tts_paged_decode_attn(const tts_attn_desc* d, int32_t num_seqs, const
   p.paged_nsplit = ns;
   p.paged_max_len = max_seq_len;
   p.q_len = 1;
+  p.two_windows = 0;
   const int64_t units = static_cast<int64_t>(num_seqs) * d->num_kv_heads * ns;
   if (units > 0x7FFFFFFF) return fail(TTS_ERR_UNSUPPORTED, "grid too large");
   hipError_t e = tts::launch_attn(p, static_cast<int>(units), d->head_dim, kv_kind(d), stream);
@@ -416,6 +417,7 @@ tts_status prefix_params(const tts_attn_desc* d, const tts_prefix_meta* m, const
   p->g = d->num_q_heads / d->num_kv_heads;
   p->scale_log2 = scale_log2(d);
   p->q_len = m->q_len;
+  p->two_windows = m->plan.two_windows ? 1 : 0;
   return TTS_OK;
 }
 

@@ -612,11 +612,18 @@ __device__ __forceinline__ void run_window(const Window& win, int n, int nt, con
 // fetched ahead of time is not waited for early) and, per lane, beam `lane`
 // (lane < 16) and entry `lane`.
 struct UnitRegs {
-  int kvh, nrows, nstatic, nent, prow0, next, mode;
+  int kvh, nrows, nstatic, nent, prow0, next, mode, nstatic2;
   int beam_l;
   int ent_id;
   uint32_t ent_inf;
 };
+
+// The record's second window (lane i: entry 64 + i), read only by units
+// that have one, when they start.
+__device__ __forceinline__ void load_window2(const UnitRec* recs, int idx, int lane, int* id, uint32_t* inf) {
+  *id = recs[idx].ent_id2[lane];
+  *inf = recs[idx].ent_info2[lane];
+}
 
 __device__ __forceinline__ int rfl(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
@@ -632,6 +639,7 @@ __device__ __forceinline__ UnitRegs load_unit(const UnitRec* recs, int idx, int 
   u.prow0 = h1.x;
   u.next = h1.y;
   u.mode = h1.z;
+  u.nstatic2 = h1.w;
   u.beam_l = r->beams[lane];
   u.ent_id = r->ent_id[lane];
   u.ent_inf = r->ent_info[lane];
@@ -703,7 +711,7 @@ __device__ __forceinline__ void store_q(const QRegs<D, KV>& qr, unsigned char* q
   }
 }
 
-template <int D, int KV>
+template <int D, int KV, bool kWin2>
 __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
   using G = Geo<D, KV>;
   using Q = QLds<D, KV>;
@@ -715,9 +723,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
   constexpr int kCombBytes = kWaves * (kTiles - 1) * G::comb_floats * 4;
   constexpr int kStageBytes = KV != kKvF32 ? 2 * Stage<D, KV>::bytes : 0;
   constexpr int kAreaBytes = kCombBytes > kStageBytes ? kCombBytes : kStageBytes;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[Q::bytes + kAreaBytes];
+  // Narrow units with a second window park its entries (per lane: block id
+  // and info word; every wave writes the same values) until the first one
+  // is done, instead of holding two more registers through the pair loop.
+  constexpr int kWin2Bytes = kWin2 ? 8 * kMaxEntries : 0;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[Q::bytes + kAreaBytes + kWin2Bytes];
   unsigned char* qbuf = lds;
   float* comb = reinterpret_cast<float*>(lds + Q::bytes);
+  uint2* win2_lds = reinterpret_cast<uint2*>(lds + Q::bytes + kAreaBytes);
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -756,6 +769,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
     u.beam_l = paged_b;
     u.ent_id = 0;
     u.ent_inf = 0;
+    u.nstatic2 = 0;
   }
   if (rfl(u.nrows) <= 0) return;
   QRegs<D, KV> qr;
@@ -818,16 +832,19 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
         unsigned char* stages = lds + Q::bytes;
         const int np = (nst + 1) >> 1;
         const int tpw = (nt + kWaves - 1) / kWaves;
-        // A wide unit has up to kMaxWideEntries blocks: entry i < 64 in lane
-        // i of ent_id, entry 64 + i in lane i of the info words (which wide
-        // units do not need). Entries (e0, e1) and block ids of pair pp; a
-        // pair never straddles the two halves.
+        // A wide unit has up to kMaxUnitEntries blocks, numbered across its
+        // two windows: entry i < 64 in lane i of ent_id, entry 64 + i in lane
+        // i of ent_id2. Entries (e0, e1) and block ids of pair pp; a pair
+        // never straddles the two windows.
+        int ent_id2 = 0;
+        uint32_t ent_inf2 = 0;
+        if (kWin2 && nst > kMaxEntries) load_window2(p.recs, rec_idx, lane, &ent_id2, &ent_inf2);
         int e0, e1, id0, id1;
         auto pair_ids = [&](int pp) {
           pp = pp < np ? pp : np - 1;  // past the end: a repeat of the last pair (a cache hit, never used)
           e0 = 2 * pp;
           e1 = 2 * pp + 1 < nst ? 2 * pp + 1 : e0;
-          const int ids = e0 < kMaxEntries ? u.ent_id : static_cast<int>(u.ent_inf);
+          const int ids = (!kWin2 || e0 < kMaxEntries) ? u.ent_id : ent_id2;
           id0 = rl(ids, e0 & (kMaxEntries - 1));
           id1 = rl(ids, e1 & (kMaxEntries - 1));
         };
@@ -839,9 +856,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             ksl = p.k_scale[u.ent_id];
             vsl = p.v_scale[u.ent_id];
           }
-          if (lane + kMaxEntries < nst) {
-            ksl2 = p.k_scale[static_cast<int>(u.ent_inf)];
-            vsl2 = p.v_scale[static_cast<int>(u.ent_inf)];
+          if (kWin2 && lane + kMaxEntries < nst) {
+            ksl2 = p.k_scale[ent_id2];
+            vsl2 = p.v_scale[ent_id2];
           }
         }
         RowState<D> st[kWideTiles];
@@ -1003,6 +1020,15 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
         win.vs = p.v_scale[win.id];
       }
     }
+    // The second window (static entries only, validated at build time) is
+    // set up when the first one is done.
+    const int nstatic2 = (!kWin2 || paged) ? 0 : rfl(u.nstatic2);
+    if (kWin2 && nstatic2 > 0) {
+      int id2;
+      uint32_t inf2;
+      load_window2(p.recs, rec_idx, lane, &id2, &inf2);
+      win2_lds[lane] = uint2{static_cast<uint32_t>(id2), inf2};
+    }
     if (!fa_ready && wave < ((nstatic + 1) >> 1))
       issue_pair<D, KV>(fa, win, nstatic, wave, kbase, vbase, blk_stride, ln, lq);
     // The next unit's record: it has this unit's pair loop to arrive.
@@ -1034,12 +1060,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
       }
       if (attempt > 0 && wave < ((nstatic + 1) >> 1))
         issue_pair<D, KV>(fa, win, nstatic, wave, kbase, vbase, blk_stride, ln, lq);
-      // Windows of blocks: the unit's own entries first, then (usually
-      // none) blocks its beams gained after the metadata was built, read
-      // from the live block table 64 at a time. One call site keeps the
-      // register allocation of the pair loop in one piece.
+      // Windows of blocks: the unit's own entries first (one or two
+      // windows), then (usually none) blocks its beams gained after the
+      // metadata was built, read from the live block table 64 at a time. One
+      // call site keeps the register allocation of the pair loop in one
+      // piece.
       Window cw = win;
       int cn = nstatic;
+      bool second = nstatic2 > 0;
       uint64_t ext_left = paged ? 0ull
                                 : __builtin_amdgcn_ballot_w64(lane >= nstatic && lane < nent &&
                                                               (u.ent_inf & kEntExt) != 0);
@@ -1047,45 +1075,59 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
       for (;;) {
         run_window<D, KV>(cw, cn, nt, kbase, vbase, blk_stride, sc, qbuf, st, fa, wave, ln, lq);
         if (attempt == 0) TTS_PROF_MARK(1, rec_idx);
-        // Next extension window, if any.
-        while (xnext >= xend && ext_left != 0) {
-          const int e = static_cast<int>(__builtin_ctzll(ext_left));
-          ext_left &= ext_left - 1;
-          xlen = rl(ext_len, e);
-          const int B = rl(ext_build, e);
-          xb = __shfl(u.beam_l, rl(u.ent_id, e) & 15);
-          xa = rl(win.a, e);
-          xe = rl(win.e, e);
-          xnext = (B + kTok - 1) / kTok;
-          xend = (xlen + kTok - 1) / kTok;
-          if (xlen < B) {
-            xend = xnext;  // shorter than at build time: the merge reports NaN
-          } else if (xend > p.max_blocks) {
-            xend = xnext;  // longer than its table row: NaN rows
+        // The next window: the unit's second one, else the next extension
+        // window; one issue site below for both.
+        int id = 0, v = 0, wa, we;
+        if (second) {
+          second = false;
+          cn = nstatic2;
+          const uint2 w2 = win2_lds[lane];
+          id = static_cast<int>(w2.x);
+          v = lane < cn ? ent_valid(w2.y) : 0;
+          wa = ent_r0(w2.y);
+          we = ent_r1(w2.y);
+        } else {
+          while (xnext >= xend && ext_left != 0) {
+            const int e = static_cast<int>(__builtin_ctzll(ext_left));
+            ext_left &= ext_left - 1;
+            xlen = rl(ext_len, e);
+            const int B = rl(ext_build, e);
+            xb = __shfl(u.beam_l, rl(u.ent_id, e) & 15);
+            xa = rl(win.a, e);
+            xe = rl(win.e, e);
+            xnext = (B + kTok - 1) / kTok;
+            xend = (xlen + kTok - 1) / kTok;
+            if (xlen < B) {
+              xend = xnext;  // shorter than at build time: the merge reports NaN
+            } else if (xend > p.max_blocks) {
+              xend = xnext;  // longer than its table row: NaN rows
+              bad_rows |= (xe >= 64 ? ~0ull : ((1ull << xe) - 1)) & ~((1ull << xa) - 1);
+            }
+          }
+          if (xnext >= xend) break;
+          cn = (xend - xnext) < kMaxEntries ? (xend - xnext) : kMaxEntries;
+          bool xbad = false;
+          if (lane < cn) {
+            const int j = xnext + lane;
+            id = p.block_tables[static_cast<int64_t>(xb / p.q_len) * p.max_blocks + j];
+            v = xlen - j * kTok;
+            v = v < kTok ? v : kTok;
+            if (id < 0 || id >= p.num_blocks) {
+              xbad = true;
+              id = 0;
+              v = 0;
+            }
+          }
+          if (__builtin_amdgcn_ballot_w64(xbad) != 0)
             bad_rows |= (xe >= 64 ? ~0ull : ((1ull << xe) - 1)) & ~((1ull << xa) - 1);
-          }
+          wa = xa;
+          we = xe;
+          xnext += cn;
         }
-        if (xnext >= xend) break;
-        cn = (xend - xnext) < kMaxEntries ? (xend - xnext) : kMaxEntries;
-        int id = 0, v = 0;
-        bool xbad = false;
-        if (lane < cn) {
-          const int j = xnext + lane;
-          id = p.block_tables[static_cast<int64_t>(xb / p.q_len) * p.max_blocks + j];
-          v = xlen - j * kTok;
-          v = v < kTok ? v : kTok;
-          if (id < 0 || id >= p.num_blocks) {
-            xbad = true;
-            id = 0;
-            v = 0;
-          }
-        }
-        if (__builtin_amdgcn_ballot_w64(xbad) != 0)
-          bad_rows |= (xe >= 64 ? ~0ull : ((1ull << xe) - 1)) & ~((1ull << xa) - 1);
         cw.id = id;
         cw.valid = v;
-        cw.a = xa;
-        cw.e = xe;
+        cw.a = wa;
+        cw.e = we;
         cw.ks = 1.f;
         cw.vs = 1.f;
         if constexpr (KV == kKvFp8) {
@@ -1094,7 +1136,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             cw.vs = p.v_scale[id];
           }
         }
-        xnext += cn;
         if (wave < ((cn + 1) >> 1)) issue_pair<D, KV>(fa, cw, cn, wave, kbase, vbase, blk_stride, ln, lq);
       }
       if (attempt > 0) break;
@@ -1468,7 +1509,10 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p) {
 
 template <int D, int KV>
 static hipError_t launch_attn_t(const AttnParams& p, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL((attn_kernel<D, KV>), dim3(grid), dim3(kThreads), 0, stream, p);
+  if (p.two_windows)
+    hipLaunchKernelGGL((attn_kernel<D, KV, true>), dim3(grid), dim3(kThreads), 0, stream, p);
+  else
+    hipLaunchKernelGGL((attn_kernel<D, KV, false>), dim3(grid), dim3(kThreads), 0, stream, p);
   return hipGetLastError();
 }
 

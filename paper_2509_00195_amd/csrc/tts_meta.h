@@ -68,6 +68,7 @@ struct WorkPlan {
   std::vector<int32_t> build_len; // [S] lengths the plan was built for
   int32_t rows_per_head = 0;      // partial rows per KV head
   int32_t num_bins = 0;
+  bool two_windows = false;       // some record has a second entry window
   int64_t num_units = 0;          // records with work
   int64_t num_slots = 0;          // slot_rows.size()
 };

@@ -79,7 +79,8 @@ struct Tmpl {
   int32_t mode = kModeNarrow;
   std::vector<int32_t> ids;
   std::vector<uint32_t> info;
-  int32_t nstatic = 0;
+  int32_t nstatic = 0;   // narrow: static entries of the first window; wide: all entries
+  int32_t nstatic2 = 0;  // narrow: entries of the second window (after the extension entries)
   double cost = 0;
   int32_t group = -1;  // wide units: index of their piece
 };
@@ -224,7 +225,7 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
         const int32_t cap = mode == kModeWide ? RW : RB;
         for (int32_t C = (G + cap - 1) / cap; C <= std::min(G, 4 * ((G + cap - 1) / cap)); ++C) {
           const int32_t rows = ((G + C - 1) / C) * g;
-          const int32_t max_ent = mode == kModeWide ? kMaxWideEntries : kMaxEntries;
+          const int32_t max_ent = mode == kModeWide ? kMaxUnitEntries : kMaxEntries;
           for (int32_t P = std::max(1, (n + max_ent - 1) / max_ent); P <= np; ++P) {
             const int32_t blocks = std::min(n, 2 * ((np + P - 1) / P));
             const double us = mode == kModeWide ? cm.wide_us(blocks, rows) : cm.narrow_us(blocks, rows);
@@ -266,18 +267,37 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
     Tmpl cur;
     std::vector<NItem> pend, ext;  // the open unit's static and extension items
     int32_t nblk = 0;
+    // A unit's entries: the first window holds its LIVE entries, static
+    // entries up to 64 with the extension entries, which come last; the
+    // second window the remaining static entries (the order of a unit's
+    // blocks does not change its result beyond rounding).
     auto flush = [&]() {
       if (pend.empty() && ext.empty()) return;
-      for (const NItem& it : pend) {
+      auto push = [&](const NItem& it) {
         cur.ids.push_back(it.id);
         cur.info.push_back(ent_info((it.p0 - cur.lo) * g, (it.p1 - cur.lo) * g, it.valid, it.flags));
+      };
+      const int32_t room1 = kMaxEntries - static_cast<int32_t>(ext.size());
+      int32_t nlive = 0;
+      for (const NItem& it : pend) nlive += (it.flags & kEntLive) ? 1 : 0;
+      int32_t plain1 = room1 - nlive;  // plain static entries the first window takes
+      std::vector<const NItem*> second;
+      for (const NItem& it : pend) {
+        if ((it.flags & kEntLive) || plain1 > 0) {
+          if (!(it.flags & kEntLive)) --plain1;
+          push(it);
+        } else {
+          second.push_back(&it);
+        }
       }
-      cur.nstatic = static_cast<int32_t>(pend.size());
+      cur.nstatic = static_cast<int32_t>(cur.ids.size());
       for (const NItem& it : ext) {
         cur.ids.push_back(it.p0 - cur.lo);
         cur.info.push_back(ent_info((it.p0 - cur.lo) * g, (it.p1 - cur.lo) * g, 1, kEntExt));
       }
-      cur.cost = cm.narrow_us(cur.nstatic, (cur.hi - cur.lo) * g);
+      for (const NItem* it : second) push(*it);
+      cur.nstatic2 = static_cast<int32_t>(second.size());
+      cur.cost = cm.narrow_us(cur.nstatic + cur.nstatic2, (cur.hi - cur.lo) * g);
       tm.push_back(std::move(cur));
       cur = Tmpl();
       pend.clear();
@@ -288,8 +308,12 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
       const bool is_ext = (it.flags & kEntExt) != 0;
       if (!pend.empty() || !ext.empty()) {
         const int32_t lo = std::min(cur.lo, it.p0), hi = std::max(cur.hi, it.p1);
-        const bool fits = hi - lo <= RB && static_cast<int32_t>(pend.size() + ext.size()) + 1 <= kMaxEntries &&
-                          cm.narrow_us(nblk + (is_ext ? 0 : 1), (hi - lo) * g) <= T;
+        int32_t nlive = 0;
+        for (const NItem& x : pend) nlive += (x.flags & kEntLive) ? 1 : 0;
+        const int32_t live_ext = nlive + static_cast<int32_t>(ext.size()) +
+                                 ((it.flags & (kEntLive | kEntExt)) ? 1 : 0);
+        const bool fits = hi - lo <= RB && static_cast<int32_t>(pend.size() + ext.size()) + 1 <= kMaxUnitEntries &&
+                          live_ext <= kMaxEntries && cm.narrow_us(nblk + (is_ext ? 0 : 1), (hi - lo) * g) <= T;
         if (!fits) flush();
       }
       if (pend.empty() && ext.empty()) {
@@ -400,7 +424,12 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
     make_templates(T, tm, ngroups);
     return static_cast<int32_t>(tm.size());
   };
+  // Upper bound of the search: a few times the average work per unit, raised
+  // while the units do not fit (one entry of many rows can cost more than
+  // that bound by its row term alone; without the raise such a batch would
+  // fall to the chained plans, with one tiny unit per entry).
   double hi = kUnitFixedUs + 4.0 * work + 1.0;
+  for (int it = 0; it < 6 && units_at(hi) > fit_units; ++it) hi *= 2.0;
   if (units_at(hi) <= fit_units) {
     double lo = kUnitFixedUs;
     for (int it = 0; it < 24; ++it) {
@@ -497,12 +526,19 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
     r.next = -1;
     r.mode = t.mode;
     for (int32_t i = 0; i < t.hi - t.lo; ++i) r.beams[i] = m.perm[t.lo + i];
+    // First window: entries [0, n1); second window: the rest.
+    const size_t n1 = t.ids.size() - static_cast<size_t>(t.mode == kModeWide ? std::max(0, t.nstatic - kMaxEntries)
+                                                                                : t.nstatic2);
+    r.nstatic2 = static_cast<int32_t>(t.ids.size() - n1);
+    if (t.mode == kModeNarrow) r.nent = static_cast<int32_t>(n1);
+    if (r.nstatic2 > 0) P.two_windows = true;
     for (size_t k = 0; k < t.ids.size(); ++k) {
-      if (k < static_cast<size_t>(kMaxEntries)) {
+      if (k < n1) {
         r.ent_id[k] = t.ids[k];
         r.ent_info[k] = t.info[k];
-      } else {  // wide units only: the second half of the block ids
-        r.ent_info[k - kMaxEntries] = static_cast<uint32_t>(t.ids[k]);
+      } else {
+        r.ent_id2[k - n1] = t.ids[k];
+        r.ent_info2[k - n1] = t.info[k];
       }
     }
     return r;

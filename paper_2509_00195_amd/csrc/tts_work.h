@@ -10,17 +10,17 @@ namespace tts {
 // One workgroup handles at most this many query rows of one KV head
 // (4 row tiles of 16); a row is one (beam, query head of the KV group).
 constexpr int kMaxRows = 64;
-// Block entries per unit (one per lane of a wave).
+// Block entries per window (one per lane of a wave). A unit has two
+// windows: the first holds its LIVE and extension entries, the second up to
+// kMaxEntries more static entries.
 constexpr int kMaxEntries = 64;
-// Wide units hold up to two per lane: entry 64 + i sits in ent_info[i].
-constexpr int kMaxWideEntries = 2 * kMaxEntries;
+constexpr int kMaxUnitEntries = 2 * kMaxEntries;
 // Beams per unit.
 constexpr int kMaxUnitBeams = 16;
 
 // Entry info word: rows [r0, r1) of the unit that attend to the block, and
 // its valid token count (static; see the flags). Wide units' blocks apply
-// to all of their rows and are full: they need no info words, and their
-// ent_info array holds the block ids of entries 64 .. 127 instead.
+// to all of their rows and are full; their info words are not read.
 //   bits  0..5   r0
 //   bits  6..11  r1 - 1
 //   bits 12..15  valid - 1
@@ -52,18 +52,20 @@ enum UnitMode : int32_t { kModeNarrow = 0, kModeWide = 1 };
 // row to partial row kvh * rows_per_head + prow0 + r.
 struct UnitRec {
   int32_t kvh;
-  int32_t nrows;    // 0: nothing to do (an idle workgroup)
-  int32_t nstatic;  // block entries (pairs are entries 2i, 2i+1); wide: up to kMaxWideEntries
-  int32_t nent;     // block entries + extension entries (these come last)
+  int32_t nrows;     // 0: nothing to do (an idle workgroup)
+  int32_t nstatic;   // first window: block entries (pairs are entries 2i, 2i+1)
+  int32_t nent;      // first window: block entries + extension entries (these come last)
   int32_t prow0;
-  int32_t next;     // next record of the same workgroup, -1 at the end
-  int32_t mode;     // UnitMode
-  int32_t pad1;
+  int32_t next;      // next record of the same workgroup, -1 at the end
+  int32_t mode;      // UnitMode
+  int32_t nstatic2;  // second window: block entries (no LIVE or extension entries)
   int32_t beams[kMaxWideBeams];  // original beam index of each unit beam
   int32_t ent_id[kMaxEntries];   // physical block id (extension: beam slot)
   uint32_t ent_info[kMaxEntries];
+  int32_t ent_id2[kMaxEntries];  // second window
+  uint32_t ent_info2[kMaxEntries];
 };
-static_assert(sizeof(UnitRec) == 32 + 4 * kMaxWideBeams + 8 * kMaxEntries, "UnitRec layout");
+static_assert(sizeof(UnitRec) == 32 + 4 * kMaxWideBeams + 16 * kMaxEntries, "UnitRec layout");
 
 // Partial softmax state of one query row over a subset of its tokens:
 // the reference maximum m (log2 units), the sum l of 2^(score - m), and
@@ -105,7 +107,9 @@ struct AttnParams {
   // virtual beam vb = b * q_len + i over beam b's table with length
   // seq_lens[b] - (q_len - 1 - i) (causal). 1 for decode.
   int32_t q_len;
-  int32_t pad2;
+  // Some unit of the plan has a second entry window: selects the kernel
+  // build that reads them (the other keeps the pair loop's registers).
+  int32_t two_windows;
 };
 
 // Slots the merge kernel reads per round trip (and the smallest slot-table
