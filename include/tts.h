@@ -164,6 +164,28 @@ tts_status tts_prefix_meta_coverage(const tts_prefix_meta* m, const int32_t* seq
  * units and partial-result slots (for diagnostics and benchmarks). */
 tts_status tts_prefix_meta_stats(const tts_prefix_meta* m, int64_t* num_units, int64_t* num_slots);
 
+/* Host-only inspection of the work plan (no device is touched): the plan
+ * tts_build_prefix_meta makes for this desc when the device has
+ * num_workgroups compute units (one persistent workgroup each), listed as
+ * one row per (unit, block entry, beam the entry applies to), 7 int32:
+ *   {unit, entry, kv_head, beam, block, valid, flags}
+ * unit numbers the units with work; entry counts across the unit's windows;
+ * beam is the original beam index; block the physical block id (-1 for an
+ * extension entry: the beam's blocks appended after the build, read from
+ * the live table at call time); valid its build-time token count (0 for
+ * extension entries). flags: 1 = the beam's partially filled last block
+ * (its valid count follows the live length), 2 = extension entry,
+ * 4 = in the unit's second window, 8 = wide unit (LDS-staged blocks that
+ * apply to all its rows). Arguments as in tts_build_prefix_meta, which
+ * validates them the same way. out_rows holds cap rows; *n_rows receives
+ * the number of rows needed and *num_units the number of units (also when
+ * cap is too small: TTS_ERR_WORKSPACE). For tests and diagnostics. */
+tts_status tts_plan_units_host(int32_t num_reqs, const int32_t* req_seq_offsets, int32_t num_seqs,
+                               const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                               int32_t block_size, int32_t num_blocks, const tts_attn_desc* desc,
+                               int32_t num_workgroups, int32_t* out_rows, int64_t cap, int64_t* n_rows,
+                               int64_t* num_units);
+
 /* Workspace bytes needed by tts_paged_decode_attn for these sizes. */
 size_t tts_paged_decode_workspace_size(const tts_attn_desc* d, int32_t num_seqs, int32_t max_seq_len);
 

@@ -31,4 +31,5 @@ from .tts import (  # noqa: F401
     tts_prefix_meta_destroy,
     tts_prefix_meta_export,
     tts_prefix_meta_stats,
+    tts_plan_units_host,
 )

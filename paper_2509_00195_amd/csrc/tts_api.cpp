@@ -270,6 +270,76 @@ tts_status tts_prefix_meta_coverage(const tts_prefix_meta* m, const int32_t* seq
   return ok();
 }
 
+tts_status tts_plan_units_host(int32_t num_reqs, const int32_t* req_seq_offsets, int32_t num_seqs,
+                               const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
+                               int32_t block_size, int32_t num_blocks, const tts_attn_desc* desc,
+                               int32_t num_workgroups, int32_t* out_rows, int64_t cap, int64_t* n_rows,
+                               int64_t* num_units) {
+  if (!desc || !n_rows || !num_units) return fail(TTS_ERR_INVALID_ARG, "NULL argument");
+  if (num_workgroups < 1) return fail(TTS_ERR_INVALID_ARG, "num_workgroups must be >= 1");
+  if (cap < 0 || (cap > 0 && !out_rows)) return fail(TTS_ERR_INVALID_ARG, "bad out_rows/cap");
+  tts_status s = check_desc(desc);
+  if (s != TTS_OK) return s;
+  if (desc->block_size != block_size) return fail(TTS_ERR_INVALID_ARG, "desc->block_size != block_size");
+  tts::MetaInput in;
+  in.num_reqs = num_reqs;
+  in.req_seq_offsets = req_seq_offsets;
+  in.num_seqs = num_seqs;
+  in.block_tables = block_tables;
+  in.max_blocks = max_blocks_per_seq;
+  in.seq_lens = seq_lens;
+  in.block_size = block_size;
+  in.num_blocks = num_blocks;
+  tts::HostMeta host;
+  tts::WorkPlan plan;
+  std::string err;
+  try {
+    const int rc = tts::build_host_meta(in, &host, &err);
+    if (rc != 0) return fail(static_cast<tts_status>(rc), err);
+    tts::build_work_plan(host, {desc->num_q_heads, desc->num_kv_heads, desc->head_dim, kv_bytes(desc), num_workgroups},
+                         &plan);
+  } catch (const std::bad_alloc&) {
+    return fail(TTS_ERR_NOMEM, "out of host memory");
+  }
+  const int32_t g = desc->num_q_heads / desc->num_kv_heads;
+  int64_t n = 0, units = 0;
+  auto emit = [&](int32_t unit, int32_t entry, int32_t kvh, int32_t beam, int32_t block, int32_t valid, int32_t flags) {
+    if (n < cap) {
+      int32_t* r = out_rows + 7 * n;
+      r[0] = unit, r[1] = entry, r[2] = kvh, r[3] = beam, r[4] = block, r[5] = valid, r[6] = flags;
+    }
+    ++n;
+  };
+  for (const tts::UnitRec& r : plan.recs) {
+    if (r.nrows <= 0) continue;
+    const int32_t u = static_cast<int32_t>(units++);
+    const int32_t nbeams = r.nrows / g;
+    if (r.mode == tts::kModeWide) {
+      for (int32_t e = 0; e < r.nstatic; ++e) {
+        const int32_t second = e >= tts::kMaxEntries;
+        const int32_t id = second ? r.ent_id2[e - tts::kMaxEntries] : r.ent_id[e];
+        for (int32_t i = 0; i < nbeams; ++i) emit(u, e, r.kvh, r.beams[i], id, block_size, 8 | (second ? 4 : 0));
+      }
+      continue;
+    }
+    for (int32_t e = 0; e < r.nent + r.nstatic2; ++e) {
+      const bool second = e >= r.nent;
+      const int32_t id = second ? r.ent_id2[e - r.nent] : r.ent_id[e];
+      const uint32_t inf = second ? r.ent_info2[e - r.nent] : r.ent_info[e];
+      const int32_t r0 = static_cast<int32_t>(inf & 63), r1 = static_cast<int32_t>((inf >> 6) & 63) + 1;
+      const bool ext = (inf & tts::kEntExt) != 0;
+      const int32_t flags = ((inf & tts::kEntLive) ? 1 : 0) | (ext ? 2 : 0) | (second ? 4 : 0);
+      const int32_t valid = ext ? 0 : static_cast<int32_t>((inf >> 12) & 15) + 1;
+      for (int32_t i = r0 / g; i < (r1 + g - 1) / g && i < nbeams; ++i)
+        emit(u, e, r.kvh, r.beams[i], ext ? -1 : id, valid, flags);
+    }
+  }
+  *n_rows = n;
+  *num_units = units;
+  if (n > cap) return fail(TTS_ERR_WORKSPACE, "cap too small for the plan rows");
+  return ok();
+}
+
 tts_status tts_prefix_meta_stats(const tts_prefix_meta* m, int64_t* num_units, int64_t* num_slots) {
   if (!m || !num_units || !num_slots) return fail(TTS_ERR_INVALID_ARG, "NULL argument");
   if (!m->has_plan) return fail(TTS_ERR_INVALID_ARG, "metadata was built without a desc");

@@ -33,7 +33,7 @@ DTYPES = {"f32": TTS_F32, "bf16": TTS_BF16, "fp8": TTS_FP8_E4M3}
 
 EXPORTED = [
     "tts_build_prefix_meta", "tts_prefix_meta_destroy", "tts_prefix_meta_export", "tts_prefix_meta_coverage",
-    "tts_prefix_meta_stats", "tts_paged_decode_workspace_size", "tts_paged_decode_attn",
+    "tts_prefix_meta_stats", "tts_plan_units_host", "tts_paged_decode_workspace_size", "tts_paged_decode_attn",
     "tts_prefix_decode_workspace_size", "tts_prefix_decode_attn", "tts_prefix_decode_partials",
     "tts_prefix_decode_merge", "tts_append_kv", "tts_copy_blocks", "tts_fork_tables", "tts_kv_alloc_time",
     "tts_kv_alloc_search", "tts_prefix_schedule", "tts_build_verify_meta", "tts_prefix_verify_attn",
@@ -112,6 +112,9 @@ def load() -> C.CDLL:
     lib.tts_prefix_meta_coverage.argtypes = [VP, pi32, pi32, I64, P(I64)]
     lib.tts_prefix_meta_stats.restype = C.c_int
     lib.tts_prefix_meta_stats.argtypes = [VP, P(I64), P(I64)]
+    lib.tts_plan_units_host.restype = C.c_int
+    lib.tts_plan_units_host.argtypes = [I32, pi32, I32, pi32, I32, pi32, I32, I32, P(tts_attn_desc), I32, pi32, I64,
+                                        P(I64), P(I64)]
     lib.tts_paged_decode_workspace_size.restype = C.c_size_t
     lib.tts_paged_decode_workspace_size.argtypes = [P(tts_attn_desc), I32, I32]
     lib.tts_paged_decode_attn.restype = C.c_int
@@ -281,6 +284,31 @@ def tts_prefix_meta_stats(meta: PrefixMeta):
     u, s = C.c_int64(0), C.c_int64(0)
     _check(load().tts_prefix_meta_stats(meta.handle, C.byref(u), C.byref(s)))
     return u.value, s.value
+
+
+# Columns of tts_plan_units_host rows, and its flags.
+PLAN_COLUMNS = ("unit", "entry", "kv_head", "beam", "block", "valid", "flags")
+PLAN_LIVE, PLAN_EXT, PLAN_SECOND, PLAN_WIDE = 1, 2, 4, 8
+
+
+def tts_plan_units_host(req_seq_offsets, block_tables, seq_lens, block_size: int, num_blocks: int,
+                        desc: tts_attn_desc, num_workgroups: int):
+    """Host-only work plan listing: (rows [n][7] int32, number of units)."""
+    lib = load()
+    offs = _host_i32(req_seq_offsets)
+    tables = _host_i32(block_tables)
+    lens = _host_i32(seq_lens)
+    s = lens.shape[0]
+    maxb = tables.shape[1] if tables.ndim == 2 else 0
+    n, units = C.c_int64(0), C.c_int64(0)
+    args = (offs.shape[0] - 1, _as_i32p(offs), s, _as_i32p(tables), maxb, _as_i32p(lens), block_size, num_blocks,
+            C.byref(desc), num_workgroups)
+    st = lib.tts_plan_units_host(*args, None, 0, C.byref(n), C.byref(units))
+    if st not in (TTS_OK, TTS_ERR_WORKSPACE):
+        _check(st)
+    rows = np.zeros((max(1, n.value), 7), np.int32)
+    _check(lib.tts_plan_units_host(*args, _as_i32p(rows), rows.shape[0], C.byref(n), C.byref(units)))
+    return rows[: n.value], units.value
 
 
 def tts_paged_decode_workspace_size(desc: tts_attn_desc, num_seqs: int, max_seq_len: int) -> int:
