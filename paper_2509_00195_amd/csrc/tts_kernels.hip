@@ -1,13 +1,16 @@
 // HIP kernels (gfx950) for prefix-shared beam decode attention.
 //
 // attn_kernel: one workgroup (4 waves) per compute unit walks a chain of
-// work units (tts_work.h). A unit holds up to 64 query rows of one KV head
-// -- whole beams, 4 row tiles of 16 -- and up to 64 KV blocks, each applying
-// to a contiguous range of the rows. Every wave keeps the softmax state of
-// ALL of the unit's rows in registers and streams its own share of the
-// unit's block pairs (pairs w, w + 4, ...) straight from HBM into registers,
-// one pair ahead of the one it computes; no LDS staging, no barriers until
-// the four waves combine their states at the end of the unit.
+// work units (tts_work.h), each the query rows of whole beams for one KV
+// head against a list of KV blocks (up to 128, in two windows of 64).
+//  * Narrow units (up to 64 rows, 4 row tiles of 16): every wave keeps the
+//    softmax state of all of the unit's rows in registers and streams its
+//    own share of the block pairs (pairs w, w + 4, ...) straight from HBM
+//    into registers, one pair ahead of the one it computes; no LDS staging
+//    and no barriers until the four waves combine their states.
+//  * Wide units (a segment shared by many beams, up to 192 rows): each block
+//    pair is loaded once, a quarter per wave, staged in LDS and read by all
+//    four waves, each running its own row tiles.
 //
 // Products on MFMA, two 16-token blocks ("a pair") at a time, per row tile:
 //   S^T = K Q^T   : 2 x 4 v_mfma_f32_16x16x32_bf16 (M = 16 tokens, N = 16
@@ -30,9 +33,9 @@
 // pairs with m_ref = that row's exact maximum. Either way each row ends
 // with a consistent (m_ref, l, o) triple.
 //
-// Every unit writes one partial softmax state (m, l, unnormalised o) per
-// row; merge_kernel combines each (beam, query head)'s states in a fixed
-// order (deterministic, no float atomics).
+// Every unit writes one partial softmax state per row; merge_row_kernel or
+// merge_kernel combines each (beam, query head)'s states in a fixed order
+// (deterministic, no float atomics).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -410,7 +413,7 @@ __device__ __forceinline__ void tile_step(const Ops<D, KV>& f, const QFrag<D, KV
 // A pair's operands are kChunks 16-byte fragments per lane (K: tile t, slice
 // j; then V: dim tile dt). Each wave loads a quarter of them (the
 // fragments of all 64 lanes, from the addresses load_pair reads) into
-// registers one pair ahead, stores them to an LDS stage -- chunk c holds
+// registers ahead of use, stores them to an LDS stage -- chunk c holds
 // fragment c of every lane, lane i at byte 16 i -- and after a barrier every
 // wave reads all chunks. (Plain loads stream faster than global-to-LDS
 // copies here.)
