@@ -11,7 +11,7 @@ step of the search); its host time is reported separately.
 Metric: beam-tokens/s = beams advanced by one token / time per layer call,
 plus the fraction of HBM peak achieved on the unique KV bytes of one call.
 
-Prints one JSON line. ``--gpus`` above 1 is refused: this build runs on one
+Prints one JSON line. ``--gpus`` above 1 is refused: the library runs on one
 GPU.
 """
 
@@ -172,7 +172,7 @@ def main():
         ingest_traffic(args)
         return
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path",
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the library has no multi-GPU path",
               file=sys.stderr)
         sys.exit(2)
     import torch

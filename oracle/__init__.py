@@ -18,6 +18,11 @@ slow and written to be checked by eye against its definitions:
   table value, appending each beam's token (with the fp8 block-scale rule),
   block copies, and the block tables of duplicated beams
   (DuplicateThenTruncate, Sec. 3.1 and Alg. 1).
+* ``schedule`` -- dynamic prefix-aware scheduling (Sec. 4.2): the greedy
+  shared-prefix order, budgeted batches and the eviction cost.
+* ``kv_alloc`` -- roofline-guided KV allocation (Sec. 4.3): the modelled
+  total time of a (prefill batch, decode batch) choice and the search over
+  the memory boundary, with a brute force over every pair.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package. The product path (the HIP library and

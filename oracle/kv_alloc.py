@@ -9,7 +9,7 @@ each batch time a roofline max(FLOPs / P, bytes / BW), under the budget
 B_pre KV_v(S) + B_dec KV_g(S_dec) <= M. The paper's search walks every
 prefill batch with the decode batch on the memory boundary and keeps the
 fastest, ties to the larger decode batch. The FLOP and byte counts of a
-stage are this build's reading of a decoder-only transformer (the paper
+stage are the reading used here of a decoder-only transformer (the paper
 only names the roofline): prefill 2 params b s + 2 L d b s (s + 1) flops
 and weights + b kv s bytes; decode 2 params b + 4 L d b c flops and
 weights + b kv c bytes. Batches are capped at N.
