@@ -315,6 +315,13 @@ def test_work_plan_stats_and_workspace():
     # every merge slot of a beam is one partial row per query head: D fp16
     # elements (bf16 cache) and four fp32 words (max, sum, row scale, pad)
     assert pref.ws_bytes >= slots * wl.shape.num_q_heads * (wl.shape.head_dim * 2 + 16)
+    # the host-only listing describes the plan the device got
+    from paper_2509_00195_amd import tts_plan_units_host
+
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+    rows, host_units = tts_plan_units_host(wl.req_seq_offsets, wl.block_tables, wl.seq_lens, 16, wl.num_blocks,
+                                           pref.desc, ncu)
+    assert host_units == units and len(rows) > 0
 
 
 def test_partials_then_merge_equals_single_call():
