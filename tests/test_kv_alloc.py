@@ -147,3 +147,58 @@ def test_search_is_fast():
     for _ in range(200):
         tts_kv_alloc_search(p)
     assert (time.perf_counter() - t0) / 200 < 1e-3
+
+
+# ---- hand-derived values (Sec. 4.3, T_tot and the roofline stage time) -------------------
+#
+# A one-layer toy pair whose counts are worked out by hand, so that a slip in the oracle's
+# arithmetic (a factor in a FLOP or byte count, s^2 for s (s + 1), c = S_dec for S_dec / 2,
+# floor for ceil in the batch counts) changes a number below.
+#   verifier : params 1000, weights 2000 B, 10 B of KV per token, L = 1, d = 4
+#   generator: params  500, weights 1000 B,  8 B of KV per token, L = 1, d = 2
+#   N = 5 requests, S = 3 verifier tokens, S_dec = 4 generated tokens (c = S_dec / 2 = 2)
+# Prefill of b = 2:  flops 2*1000*2*3 + 2*1*4*2*3*(3+1) = 12000 + 192 = 12192
+#                    bytes 2000 + 2*10*3 = 2060;   ceil(5/2) = 3 batches
+# Decode of b = 3:   flops 2*500*3 + 4*1*2*3*2 = 3000 + 48 = 3048
+#                    bytes 1000 + 3*8*2 = 1048;    ceil(5/3) = 2 batches, S_dec = 4 steps each
+# Memory-bound rates (P = 1000 flop/s, BW = 100 B/s): prefill max(12.192, 20.6) = 20.6 s,
+#   T_pre = 3 * 20.6 = 61.8; decode max(3.048, 10.48) = 10.48 s, T_dec = 2 * 4 * 10.48 = 83.84.
+# Compute-bound rates (P = 100 flop/s, BW = 1000 B/s): prefill max(121.92, 2.06) = 121.92,
+#   T_pre = 365.76; decode max(30.48, 1.048) = 30.48, T_dec = 243.84.
+
+def _toy(pf, bw, mem=1e9):
+    v = ModelCost(1000.0, 2000.0, 10.0, 1, 4)
+    g = ModelCost(500.0, 1000.0, 8.0, 1, 2)
+    return AllocProblem(v, g, 5, 3, 4, mem, pf, bw)
+
+
+@pytest.mark.parametrize("pf,bw,want", [
+    (1000.0, 100.0, (61.8 + 83.84, 61.8, 83.84)),     # both stages memory-bound
+    (100.0, 1000.0, (365.76 + 243.84, 365.76, 243.84)),  # both stages compute-bound
+])
+def test_total_time_hand_derived(pf, bw, want):
+    p = _toy(pf, bw)
+    assert total_time(p, 2, 3) == pytest.approx(want, rel=1e-12)
+    t = tts_kv_alloc_time(_lib(p), 2, 3)
+    assert (t.t_tot, t.t_pre, t.t_dec) == pytest.approx(want, rel=1e-12)
+
+
+def test_search_hand_derived():
+    """M = 130 B; one prefill sequence holds 10*3 = 30 B, one decode sequence 8*4 = 32 B.
+    Memory-bound rates (P = 1000, BW = 100), the decode batch on the boundary:
+      B_pre 1: B_dec = floor(100/32) = 3; prefill(1) max(6096/1000, 2030/100) = 20.3, 5 batches
+               = 101.5; decode(3) = 83.84 (above)                            T_tot = 185.34
+      B_pre 2: B_dec = floor(70/32) = 2; 61.8 + decode(2): max(2032/1000, 1032/100) = 10.32,
+               ceil(5/2) * 4 * 10.32 = 123.84                                 T_tot = 185.64
+      B_pre 3: B_dec = floor(40/32) = 1; prefill(3) max(18288/1000, 2090/100) = 20.9, 2 batches
+               = 41.8; decode(1) max(1016/1000, 1016/100) = 10.16, 5 * 4 * 10.16 = 203.2
+                                                                              T_tot = 245.0
+      B_pre 4: 130 - 120 = 10 B leaves no room for a decode sequence: the search stops.
+    The best pair is (1, 3) at 185.34 s."""
+    p = _toy(1000.0, 100.0, mem=130.0)
+    bp, bd, t = search(p)
+    assert (bp, bd) == (1, 3) and t == pytest.approx(185.34, rel=1e-12)
+    assert total_time(p, 2, 2)[0] == pytest.approx(185.64, rel=1e-12)
+    assert total_time(p, 3, 1)[0] == pytest.approx(245.0, rel=1e-12)
+    got = tts_kv_alloc_search(_lib(p))
+    assert (got.b_pre, got.b_dec) == (1, 3) and got.t_tot == pytest.approx(185.34, rel=1e-12)

@@ -111,3 +111,43 @@ def test_schedule_is_the_metadata_beam_order(name):
     order, _, _, _ = tts_prefix_schedule(cots, 10 ** 8 + w.num_seqs, 10 ** 9)
     meta = oracle_prefix_meta(w.req_seq_offsets, w.block_tables, w.seq_lens, 16)
     assert order.tolist() == list(meta["perm"])
+
+
+# ---- hand-derived values (Sec. 4.2: Cost = sum_i Nodes(T_i) - P(T_i, T_{i+1})) -----------
+#
+# Five CoTs (node-id paths): c0 = [1,2,3], c1 = [1,5], c2 = [1,2,6], c3 = [1,2,7], c4 = [1,8].
+GOLD_COTS = [[1, 2, 3], [1, 5], [1, 2, 6], [1, 2, 7], [1, 8]]
+
+
+def test_eviction_cost_hand_derived():
+    """CoTs c0 = [1,2,3], c1 = [1,4], c2 = [1,4,5], c3 = [1,6], c4 = [1,2,7] in the batches
+    [c0 c3 c4], [c1], [c2]: tries T0 = {1,2,3,6,7}, T1 = {1,4}, T2 = {1,4,5};
+    T0 & T1 = {1}, T1 & T2 = {1,4}, and the last trie has no successor.
+    Unit weights: (5 - 1) + (2 - 2) + (3 - 0) = 7. With weight(v) = v: T0 = 19, T1 = 5,
+    T2 = 10, overlaps 1 and 5: (19 - 1) + (5 - 5) + 10 = 28.
+    Slips this separates: the previous trie's overlap instead of the next one's gives 8, the
+    last trie's overlap with the first 6, dropping the last trie 4, summing per CoT instead of
+    per trie (3 + 2 + 3 + 2 + 3 - 1 - 1 - 1 - 2) 8."""
+    cots = [[1, 2, 3], [1, 4], [1, 4, 5], [1, 6], [1, 2, 7]]
+    bl = [[0, 3, 4], [1], [2]]
+    assert eviction_cost(bl, cots) == 7
+    assert eviction_cost(bl, cots, list(range(8))) == 28
+
+
+def test_schedule_hand_derived():
+    """Greedy from c0 = [1,2,3]: shared prefixes with c1..c4 are 1, 2, 2, 1 -> c2 (earliest
+    of the ties); from c2: c1 1, c3 2, c4 1 -> c3; from c3: c1 1, c4 1 -> c1; then c4.
+    Order [0, 2, 3, 1, 4], score 2 + 2 + 1 + 1 = 6.
+    Budget 5 (unit weights): c0 -> 3 nodes, + c2 -> 4, + c3 -> {1,2,3,6,7} = 5, + c1 would be
+    6 > 5, so the batches are [0 2 3], [1 4] ({1,5,8}); cost (5 - |{1}|) + 3 = 7.
+    Budget 20 with weight(v) = v: 6, 12, 19, then + 5 = 24 > 20; same batches; cost
+    (19 - 1) + (1 + 5 + 8) = 32."""
+    assert greedy_order(GOLD_COTS) == [0, 2, 3, 1, 4]
+    assert score([0, 2, 3, 1, 4], GOLD_COTS) == 6
+    assert batches([0, 2, 3, 1, 4], GOLD_COTS, 5) == [[0, 2, 3], [1, 4]]
+    assert batches([0, 2, 3, 1, 4], GOLD_COTS, 20, list(range(9))) == [[0, 2, 3], [1, 4]]
+    assert eviction_cost([[0, 2, 3], [1, 4]], GOLD_COTS) == 7
+    order, bl, sc, co = tts_prefix_schedule(GOLD_COTS, 9, 5)
+    assert order.tolist() == [0, 2, 3, 1, 4] and bl == [[0, 2, 3], [1, 4]] and sc == 6 and co == 7
+    order, bl, sc, co = tts_prefix_schedule(GOLD_COTS, 9, 20, list(range(9)))
+    assert bl == [[0, 2, 3], [1, 4]] and co == 32
