@@ -29,9 +29,13 @@
 // cross-lane reductions, no accumulator rescaling and no data-dependent
 // branches. Each lane tracks the largest score it has seen; if a row's
 // maximum leaves [-kRefWindow, kRefWindow] (where exp2 could overflow the
-// fp32 accumulators or underflow every weight), the wave recomputes its
-// pairs with m_ref = that row's exact maximum. Either way each row ends
-// with a consistent (m_ref, l, o) triple.
+// fp32 accumulators or underflow every weight), its pairs are computed again
+// with m_ref = that row's exact maximum: per wave in narrow units (no
+// barrier inside their loop), by the whole workgroup in wide units (whose
+// loop holds barriers, so the decision is taken over all four waves).
+// Either way each row ends with a consistent (m_ref, l, o) triple; a state
+// that saw no token (l = 0) carries m = -inf, so it never sets the maximum
+// of a combine or a merge.
 //
 // Every unit writes one partial softmax state per row; merge_row_kernel or
 // merge_kernel combines each (beam, query head)'s states in a fixed order
@@ -162,8 +166,11 @@ __device__ __forceinline__ void write_partial(void* part_o, float* part_ml, int6
 #pragma unroll
     for (int t = 0; t < D / 16; ++t) dst[t] = o[t] * inv;
   }
+  // A state without tokens (l = 0) takes no part in the merge's maximum; a
+  // NaN m (a bad row) is kept.
+  const float m_out = (l > 0.f || m != m) ? m : kNegInf;
   if (lq == 0)
-    *reinterpret_cast<f32x4*>(part_ml + prow * kPartMl) = f32x4{m, l, __builtin_ldexpf(1.f, e), 0.f};
+    *reinterpret_cast<f32x4*>(part_ml + prow * kPartMl) = f32x4{m_out, l, __builtin_ldexpf(1.f, e), 0.f};
 }
 
 __device__ __forceinline__ int rl(int x, int i) { return __builtin_amdgcn_readlane(x, i); }
@@ -730,10 +737,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
   // and info word; every wave writes the same values) until the first one
   // is done, instead of holding two more registers through the pair loop.
   constexpr int kWin2Bytes = kWin2 ? 8 * kMaxEntries : 0;
-  __shared__ __attribute__((aligned(16))) unsigned char lds[Q::bytes + kAreaBytes + kWin2Bytes];
+  // Wide units: each wave's "redo" vote (one word per wave).
+  constexpr int kVoteBytes = 4 * kWaves;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[Q::bytes + kAreaBytes + kWin2Bytes + kVoteBytes];
   unsigned char* qbuf = lds;
   float* comb = reinterpret_cast<float*>(lds + Q::bytes);
   uint2* win2_lds = reinterpret_cast<uint2*>(lds + Q::bytes + kAreaBytes);
+  int* votes = reinterpret_cast<int*>(lds + Q::bytes + kAreaBytes + kWin2Bytes);
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -954,7 +964,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             redo |= mx > kRefWindow || (mx < -kRefWindow && mx != kNegInf);
             m_exact[i] = mx == kNegInf ? 0.f : mx;
           }
-          if (__builtin_amdgcn_ballot_w64(redo) == 0) break;
+          // The loop holds barriers, so every wave repeats it or none does:
+          // each wave votes, and all four read every vote. (The votes are
+          // written again only after the next unit's first barrier.)
+          const bool wave_redo = __builtin_amdgcn_ballot_w64(redo) != 0;
+          if (lane == 0) votes[wave] = wave_redo ? 1 : 0;
+          __syncthreads();
+          if ((votes[0] | votes[1] | votes[2] | votes[3]) == 0) break;
         }
         // Each wave writes the partial states of its own rows.
 #pragma unroll
@@ -1185,10 +1201,16 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
       if (r != wave || r >= nt) continue;
       const int row = 16 * r + ln;
       const float own_l = xlane_sum16(st[r].l);
-      float mw[kWaves], mx = kNegInf;
+      // A wave that saw no token of the row (l = 0: no pair of it, or every
+      // score masked) keeps its initial reference; it must not set the
+      // maximum, or a row whose scores all lie far below it would lose every
+      // weight to underflow.
+      float mw[kWaves], lw[kWaves], mx = kNegInf;
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
-        mw[w] = (w == r) ? st[r].m : comb_slot(w, r)[kTok * G::comb_row + ln];
+        lw[w] = (w == r) ? own_l : comb_slot(w, r)[kTok * G::comb_row + kTok + ln];
+        const float m = (w == r) ? st[r].m : comb_slot(w, r)[kTok * G::comb_row + ln];
+        mw[w] = lw[w] > 0.f ? m : kNegInf;
         mx = fmaxf(mx, mw[w]);
       }
       float l = 0.f;
@@ -1197,14 +1219,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
       for (int dt = 0; dt < D / 16; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int w = 0; w < kWaves; ++w) {
-        const float f = __builtin_amdgcn_exp2f(mw[w] - mx);
+        const float f = mw[w] == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mw[w] - mx);
         if (w == r) {
           l += own_l * f;
 #pragma unroll
           for (int dt = 0; dt < D / 16; ++dt) o[dt] += st[r].o[dt] * f;
         } else {
           const float* c = comb_slot(w, r);
-          l += c[kTok * G::comb_row + kTok + ln] * f;
+          l += lw[w] * f;
 #pragma unroll
           for (int dt = 0; dt < D / 16; ++dt)
             o[dt] += *reinterpret_cast<const f32x4*>(c + ln * G::comb_row + 16 * dt + 4 * lq) * f;
@@ -1295,8 +1317,9 @@ struct MergeRaw<4, false> {
 };
 
 // Exact merge of the partial softmax states of each (beam, query head), in
-// the order of the beam's slot list. With M = max_k m_k and
-// w_k = l_k 2^(m_k - M), and e_k the stored elements o_k / (l_k s_k):
+// the order of the beam's slot list. With M = max_k m_k over the states
+// that saw tokens (l_k > 0), w_k = l_k 2^(m_k - M), and e_k the stored
+// elements o_k / (l_k s_k):
 //   out = sum_k w_k s_k e_k / sum_k w_k.
 // Two kernels compute it; launch_merge picks by the number of rows.
 //
@@ -1364,8 +1387,10 @@ __global__ __launch_bounds__(kThreads) void merge_row_kernel(MergeParams p) {
       for (int k = 0; k < kBatch; ++k) ent[k] = k0 + kBatch + k < n ? tab[1 + k0 + kBatch + k] : 0;
     }
 #pragma unroll
-    for (int k = 0; k < kBatch; ++k)
+    for (int k = 0; k < kBatch; ++k) {
       if (k0 + k >= n) ml[k] = f32x4{kNegInf, 0.f, 0.f, 0.f};
+      if (ml[k].y == 0.f && ml[k].x == ml[k].x) ml[k].x = kNegInf;  // a state without tokens
+    }
     float bm = kNegInf;
 #pragma unroll
     for (int k = 0; k < kBatch; ++k) {
@@ -1467,6 +1492,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p) {
       raw[k] = MergeRaw<kEpl, F16>::load(p.part_o, static_cast<int64_t>(row_k) * D + kEpl * j);
     }
     if (!has) ml = f32x4{kNegInf, 0.f, 0.f, 0.f};
+    if (ml.y == 0.f && ml.x == ml.x) ml.x = kNegInf;  // a state without tokens
     nan |= ml.x != ml.x;
     float bm = ml.x;
 #pragma unroll

@@ -17,6 +17,7 @@ from paper_2509_00195_amd import TTSError
 from paper_2509_00195_amd.runner import PagedAttention, PrefixAttention
 from tts_synth import CONFIGS, AttnShape, BeamTree, make_workload, workload_from_tree
 from tts_synth.device import to_device
+from tests._paged import bf16_bits
 
 pytestmark = pytest.mark.gpu
 
@@ -64,41 +65,41 @@ def test_parity_configs(name, seed):
     assert err(ox, ref) <= tol
 
 
-def test_parity_straggler():
-    wl = make_workload("7b_straggler", 0)
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_parity_straggler(seed):
+    wl = make_workload("7b_straggler", seed)
     ref = oracle_attn_workload(wl)
     op, ox = outputs(wl)
-    print(f"straggler: paged {err(op, ref):.2e} prefix {err(ox, ref):.2e}", flush=True)
+    print(f"straggler seed {seed}: paged {err(op, ref):.2e} prefix {err(ox, ref):.2e}", flush=True)
+    assert np.isfinite(op).all() and np.isfinite(ox).all()
     assert err(op, ref) <= TOL["bf16"] and err(ox, ref) <= TOL["bf16"]
 
 
-def test_parity_balanced_tree():
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_parity_balanced_tree(seed):
     """The low-sharing balanced tree (long private tails)."""
-    wl = make_workload("7b64_balanced", 0)
+    wl = make_workload("7b64_balanced", seed)
     ref = oracle_attn_workload(wl)
     op, ox = outputs(wl)
-    print(f"balanced: paged {err(op, ref):.2e} prefix {err(ox, ref):.2e}", flush=True)
+    print(f"balanced seed {seed}: paged {err(op, ref):.2e} prefix {err(ox, ref):.2e}", flush=True)
+    assert np.isfinite(op).all() and np.isfinite(ox).all()
     assert err(op, ref) <= TOL["bf16"] and err(ox, ref) <= TOL["bf16"]
 
 
-@pytest.mark.parametrize("kv", ["fp8", "bf16"])
-def test_parity_longchain_sampled(kv):
-    """The long-chain batch at full size (its wide units hold up to 128 blocks,
-    ids 64.. in the info words), in fp8 as configured and in bf16."""
+@pytest.mark.parametrize("kv,seed", [("fp8", 0), ("fp8", 1), ("fp8", 2), ("bf16", 0)])
+def test_parity_longchain(kv, seed):
+    """The long-chain batch at full size (its wide units hold up to 128 blocks, ids 64.. in the
+    info words), every beam against the oracle: fp8 as configured (seeds 0-2) and bf16."""
     cfg = CONFIGS["7b_longchain_fp8"]
     if kv != "fp8":
         cfg = dataclasses.replace(cfg, shape=dataclasses.replace(cfg.shape, kv_dtype=kv))
-    wl = make_workload(cfg, 0)
-    s = wl.num_seqs
-    rng = np.random.default_rng(0)
-    rows = sorted(set(rng.choice(s, 20, replace=False).tolist()) | {int(np.argmax(wl.seq_lens)), 0, s - 1})
-    ref = oracle_attn_workload(wl, beams=rows)
+    wl = make_workload(cfg, seed)
     op, ox = outputs(wl)
-    print(f"longchain {kv} ({len(rows)} beams): paged {err(op, ref, rows):.2e} prefix {err(ox, ref, rows):.2e}",
-          flush=True)
     assert np.isfinite(op).all() and np.isfinite(ox).all()
-    assert err(op, ref, rows) <= TOL[kv] and err(ox, ref, rows) <= TOL[kv]
-    assert err(op, ox) <= TOL[kv]  # every beam: the two paths agree
+    ref = oracle_attn_workload(wl)
+    print(f"longchain {kv} seed {seed} (all {wl.num_seqs} beams): paged {err(op, ref):.2e} "
+          f"prefix {err(ox, ref):.2e}", flush=True)
+    assert err(op, ref) <= TOL[kv] and err(ox, ref) <= TOL[kv]
 
 
 def test_run_to_run_deterministic():
@@ -336,3 +337,39 @@ def test_partials_then_merge_equals_single_call():
     tts_prefix_decode_merge(pref.desc, pref.meta, x.seq_lens, out, pref.ws, pref.ws_bytes)
     torch.cuda.synchronize()
     assert torch.equal(out, ref)
+
+
+# Error relative to the values, for bf16 and fp8 caches. The value product takes the
+# probabilities rounded to bf16 (relative error <= 2^-9 each; the row is a convex combination
+# of value rows, so at most 2^-9 max|V| in total), and each partial state is stored as fp16
+# elements of magnitude <= 1 times a power-of-two row scale s < 2 max|partial row| (absolute
+# error <= 2^-12 s < 2^-11 max|V|, carried through the merge's weights, which sum to 1); fp32
+# accumulation and the scores add about 1e-6 relative. Hence, per beam,
+#   max |out - oracle| <= (2^-9 + 2^-11 + 2^-14) max|V over the beam's tokens|,
+# which the N(0, 1) tolerance of 1e-2 does not state for values of any size.
+REL_BOUND = 2.0 ** -9 + 2.0 ** -11 + 2.0 ** -14
+
+
+def _heavy_tailed_values(wl, seed):
+    """Values with heavy tails: a tenth of the (block, slot) tokens scaled x30 and the rest
+    scaled by |t(3)| draws per token (unused slots keep their NaN)."""
+    rng = np.random.default_rng(seed)
+    v = torch.from_numpy(wl.v_cache.view(np.int16)).view(torch.bfloat16).float().numpy()  # [nb][Hkv][D][16]
+    nb = v.shape[0]
+    f = np.abs(rng.standard_t(3, size=(nb, 1, 1, 16))) + 0.1
+    f = np.where(rng.random((nb, 1, 1, 16)) < 0.1, 30.0, f)
+    return dataclasses.replace(wl, v_cache=bf16_bits(v * f))
+
+
+@pytest.mark.parametrize("name", ["7b64", "1p5b16"])
+def test_error_relative_to_values_heavy_tails(name):
+    wl = _heavy_tailed_values(make_workload(name, 0), 21)
+    ref = oracle_attn_workload(wl)
+    op, ox = outputs(wl)
+    worst = 0.0
+    for b in range(wl.num_seqs):
+        vmax = _max_abs_v(wl, b)
+        eb = max(err(op[b], ref[b]), err(ox[b], ref[b]))
+        worst = max(worst, eb / vmax)
+        assert eb <= REL_BOUND * vmax, (b, eb, vmax)
+    print(f"{name} heavy-tailed values: worst error / max|V| = {worst:.2e} (bound {REL_BOUND:.2e})", flush=True)
