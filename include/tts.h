@@ -230,6 +230,25 @@ tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta*
                                   const int32_t* seq_lens, int32_t num_blocks, void* out, void* workspace,
                                   size_t workspace_bytes, hipStream_t stream);
 
+/* For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.
+ * tts_prefix_decode_attn without a workspace argument; arguments, rules and
+ * results are those of tts_prefix_decode_attn (same kernels, same plan).
+ * The partial softmax states go to a scratch array of 64 MiB that the
+ * library holds on each GPU it runs on, from the first call on that GPU
+ * until the process ends; nothing is allocated or freed (no hipMalloc,
+ * hipFree or allocating library call). A metadata whose
+ * tts_prefix_decode_workspace_size exceeds 64 MiB is refused with
+ * TTS_ERR_WORKSPACE before anything is enqueued. Every call on one GPU uses
+ * that GPU's one array: calls that overlap in time on the same GPU (two
+ * streams, or two host threads) race on it and must be serialised by the
+ * caller. */
+tts_status tts_prefix_decode_attn_noalloc(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
+                                          const void* k_cache, const void* v_cache, const float* k_scale,
+                                          const float* v_scale, const int32_t* block_tables,
+                                          int32_t max_blocks_per_seq, const int32_t* seq_lens, int32_t num_blocks,
+                                          void* out, hipStream_t stream);
+
 /* ---- Verification attention over the shared prefix (LookAhead
  * Verification, Sec. 4.1: the current and the speculative step go to the
  * verifier as one request; its attention is a multi-token causal attention

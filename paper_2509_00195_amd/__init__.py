@@ -24,6 +24,7 @@ from .tts import (  # noqa: F401
     tts_paged_decode_attn,
     tts_paged_decode_workspace_size,
     tts_prefix_decode_attn,
+    tts_prefix_decode_attn_noalloc,
     tts_prefix_decode_merge,
     tts_prefix_decode_partials,
     tts_prefix_decode_workspace_size,

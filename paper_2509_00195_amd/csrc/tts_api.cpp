@@ -17,6 +17,7 @@
 namespace tts {
 hipError_t launch_attn(const AttnParams& p, int grid, int head_dim, int kv_kind, hipStream_t stream);
 hipError_t launch_merge(const MergeParams& p, int head_dim, int kv_kind, hipStream_t stream);
+hipError_t scratch_buffer(void** ptr, size_t* bytes);
 hipError_t launch_append(const void* k_new, const void* v_new, const int32_t* block_tables, const int32_t* seq_lens,
                          void* k_cache, void* v_cache, float* k_scale, float* v_scale, int num_seqs, int max_blocks,
                          int num_blocks, int hkv, int head_dim, int kv_kind, hipStream_t stream);
@@ -531,6 +532,34 @@ tts_status tts_prefix_decode_attn(const tts_attn_desc* d, const tts_prefix_meta*
   tts::AttnParams p;
   tts_status s = prefix_params(d, m, q, k_cache, v_cache, k_scale, v_scale, block_tables, max_blocks_per_seq,
                                seq_lens, num_blocks, out, workspace, workspace_bytes, true, &p);
+  if (s != TTS_OK || m->host.num_seqs == 0) return s == TTS_OK ? ok() : s;
+  if ((s = launch_partials(d, m, p, stream)) != TTS_OK) return s;
+  if ((s = launch_prefix_merge(d, m, p, stream)) != TTS_OK) return s;
+  return ok();
+}
+
+tts_status tts_prefix_decode_attn_noalloc(const tts_attn_desc* d, const tts_prefix_meta* m, const void* q,
+                                          const void* k_cache, const void* v_cache, const float* k_scale,
+                                          const float* v_scale, const int32_t* block_tables,
+                                          int32_t max_blocks_per_seq, const int32_t* seq_lens, int32_t num_blocks,
+                                          void* out, hipStream_t stream) {
+  if (m && m->q_len != 1)
+    return fail(TTS_ERR_INVALID_ARG, "verification metadata (q_len > 1): use tts_prefix_verify_attn");
+  // The library's own scratch array on the current device (no allocation).
+  void* scratch = nullptr;
+  size_t scratch_bytes = 0;
+  const hipError_t e = tts::scratch_buffer(&scratch, &scratch_bytes);
+  if (e != hipSuccess) return fail(TTS_ERR_HIP, std::string("scratch lookup: ") + hipGetErrorString(e));
+  if (d && m && m->has_plan && check_desc(d) == TTS_OK) {
+    const size_t need = tts_prefix_decode_workspace_size(d, m);
+    if (need > scratch_bytes)
+      return fail(TTS_ERR_WORKSPACE, "the plan needs " + std::to_string(need) + " bytes of partial states; the "
+                  "allocation-free call holds " + std::to_string(scratch_bytes) + " (use tts_prefix_decode_attn "
+                  "with a workspace)");
+  }
+  tts::AttnParams p;
+  tts_status s = prefix_params(d, m, q, k_cache, v_cache, k_scale, v_scale, block_tables, max_blocks_per_seq,
+                               seq_lens, num_blocks, out, scratch, scratch_bytes, true, &p);
   if (s != TTS_OK || m->host.num_seqs == 0) return s == TTS_OK ? ok() : s;
   if ((s = launch_partials(d, m, p, stream)) != TTS_OK) return s;
   if ((s = launch_prefix_merge(d, m, p, stream)) != TTS_OK) return s;

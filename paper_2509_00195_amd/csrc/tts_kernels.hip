@@ -43,6 +43,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 #include <type_traits>
 
 #include "tts_work.h"
@@ -1591,6 +1592,38 @@ hipError_t launch_attn(const AttnParams& p, int grid, int head_dim, int kv_kind,
   if (kv_kind == kKvBf16) return launch_attn_t<64, kKvBf16>(p, grid, stream);
   if (kv_kind == kKvFp8) return launch_attn_t<64, kKvFp8>(p, grid, stream);
   return launch_attn_t<64, kKvF32>(p, grid, stream);
+}
+
+// ---- scratch of the allocation-free entry point ----------------------------
+// Partial softmax states of one prefix-attention call for callers that cannot
+// allocate device memory. The array is part of the code object: every GPU
+// the library runs on holds its own copy, at its own address, until the
+// process ends. In host code the name `scratch` is only a stand-in; the
+// device address comes from hipGetSymbolAddress, looked up once per device
+// with that device current.
+constexpr size_t kScratchBytes = size_t{64} << 20;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kScratchMaxDevices = 64;
+
+hipError_t scratch_buffer(void** ptr, size_t* bytes) {
+  static std::mutex mu;
+  static void* dev_ptr[kScratchMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!dev_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    dev_ptr[dev] = p;
+  }
+  *ptr = dev_ptr[dev];
+  *bytes = kScratchBytes;
+  return hipSuccess;
 }
 
 }  // namespace tts

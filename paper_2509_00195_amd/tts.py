@@ -34,7 +34,8 @@ DTYPES = {"f32": TTS_F32, "bf16": TTS_BF16, "fp8": TTS_FP8_E4M3}
 EXPORTED = [
     "tts_build_prefix_meta", "tts_prefix_meta_destroy", "tts_prefix_meta_export", "tts_prefix_meta_coverage",
     "tts_prefix_meta_stats", "tts_plan_units_host", "tts_paged_decode_workspace_size", "tts_paged_decode_attn",
-    "tts_prefix_decode_workspace_size", "tts_prefix_decode_attn", "tts_prefix_decode_partials",
+    "tts_prefix_decode_workspace_size", "tts_prefix_decode_attn", "tts_prefix_decode_attn_noalloc",
+    "tts_prefix_decode_partials",
     "tts_prefix_decode_merge", "tts_append_kv", "tts_copy_blocks", "tts_fork_tables", "tts_kv_alloc_time",
     "tts_kv_alloc_search", "tts_prefix_schedule", "tts_build_verify_meta", "tts_prefix_verify_attn",
     "tts_last_error",
@@ -127,6 +128,9 @@ def load() -> C.CDLL:
                                            C.c_size_t, VP]
     lib.tts_prefix_verify_attn.restype = C.c_int
     lib.tts_prefix_verify_attn.argtypes = lib.tts_prefix_decode_attn.argtypes
+    lib.tts_prefix_decode_attn_noalloc.restype = C.c_int
+    lib.tts_prefix_decode_attn_noalloc.argtypes = [P(tts_attn_desc), VP, VP, VP, VP, VP, VP, VP, I32, VP, I32, VP,
+                                                   VP]
     lib.tts_prefix_decode_partials.restype = C.c_int
     lib.tts_prefix_decode_partials.argtypes = lib.tts_prefix_decode_attn.argtypes
     lib.tts_prefix_decode_merge.restype = C.c_int
@@ -336,6 +340,14 @@ def tts_prefix_decode_attn(desc: tts_attn_desc, meta: PrefixMeta, q, k_cache, v_
         _ptr(block_tables), max_blocks_per_seq, _ptr(seq_lens), num_blocks, _ptr(out), _ptr(workspace),
         workspace_bytes, _stream(stream)))
 
+
+
+def tts_prefix_decode_attn_noalloc(desc: tts_attn_desc, meta: PrefixMeta, q, k_cache, v_cache, k_scale, v_scale,
+                                   block_tables, max_blocks_per_seq: int, seq_lens, num_blocks: int, out,
+                                   stream=None):
+    _check(load().tts_prefix_decode_attn_noalloc(
+        C.byref(desc), meta.handle, _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(k_scale), _ptr(v_scale),
+        _ptr(block_tables), max_blocks_per_seq, _ptr(seq_lens), num_blocks, _ptr(out), _stream(stream)))
 
 
 def tts_prefix_decode_partials(desc: tts_attn_desc, meta: PrefixMeta, q, k_cache, v_cache, k_scale, v_scale,
