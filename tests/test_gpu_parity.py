@@ -373,3 +373,29 @@ def test_error_relative_to_values_heavy_tails(name):
         worst = max(worst, eb / vmax)
         assert eb <= REL_BOUND * vmax, (b, eb, vmax)
     print(f"{name} heavy-tailed values: worst error / max|V| = {worst:.2e} (bound {REL_BOUND:.2e})", flush=True)
+
+
+def test_one_workspace_across_batches():
+    """A search loop rebuilds its metadata every iteration and keeps its workspace: one
+    workspace, filled with garbage first, serves two batches' metadata in turn (A, B, A, B).
+    Every call meets the oracle, and the full call equals its partials + merge launches."""
+    from paper_2509_00195_amd import tts_prefix_decode_attn, tts_prefix_decode_merge, tts_prefix_decode_partials
+
+    runs = []
+    for seed in (0, 1):
+        wl = make_workload("7b64", seed)
+        x, _, pref = runners(wl)
+        runs.append((wl, x, pref, oracle_attn_workload(wl)))
+    nbytes = max(r[2].ws_bytes for r in runs)
+    ws = torch.full((nbytes,), 0xA5, dtype=torch.uint8, device="cuda:0")
+    for wl, x, pref, ref in runs + runs:
+        args = (pref.desc, pref.meta, x.q, x.k_cache, x.v_cache, None, None, x.block_tables,
+                x.block_tables.shape[1], x.seq_lens, wl.num_blocks)
+        one = torch.full_like(pref.out, float("nan"))
+        two = torch.full_like(pref.out, float("nan"))
+        tts_prefix_decode_attn(*args, one, ws, nbytes)
+        tts_prefix_decode_partials(*args, two, ws, nbytes)
+        tts_prefix_decode_merge(pref.desc, pref.meta, x.seq_lens, two, ws, nbytes)
+        torch.cuda.synchronize()
+        assert torch.equal(one, two)
+        assert err(one.cpu().numpy(), ref) <= TOL["bf16"]
