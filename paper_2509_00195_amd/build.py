@@ -60,5 +60,37 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
     return out
 
 
+SANITIZE = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer", "-g", "-O1"]
+
+
+def build_sanitized(out: str, verbose: bool = False) -> str:
+    """A CPU-test build of the library: the host sources (metadata, planner,
+    scheduler, allocation search, C ABI) compiled by g++ with AddressSanitizer
+    and UndefinedBehaviorSanitizer, the HIP sources compiled as usual (their
+    kernels are not run by the host tests). Load it with the ASan runtime
+    preloaded (``g++ -print-file-name=libasan.so``)."""
+    gxx = os.environ.get("CXX_HOST", "g++")
+    host_flags = ["-std=c++17", "-fPIC", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include",
+                  f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}", *SANITIZE]
+    with tempfile.TemporaryDirectory(prefix="tts_san_") as tmp:
+        objs = []
+        for src in SOURCES_HIP:
+            obj = os.path.join(tmp, src + ".o")
+            _run([HIPCC, *COMMON, *DEVICE, "-c", os.path.join(CSRC, src), "-o", obj])
+            objs.append(obj)
+        for src in SOURCES_HOST:
+            obj = os.path.join(tmp, src + ".o")
+            _run([gxx, *host_flags, "-c", os.path.join(CSRC, src), "-o", obj])
+            objs.append(obj)
+        out_tmp = os.path.join(tmp, "libtts_san.so")
+        _run([gxx, "-shared", "-fPIC", *SANITIZE, *objs, "-L/opt/rocm/lib", "-lamdhip64",
+              "-Wl,-rpath,/opt/rocm/lib", "-o", out_tmp])
+        shutil.copyfile(out_tmp, out + ".tmp")
+        os.replace(out + ".tmp", out)
+    if verbose:
+        print(f"built {out}")
+    return out
+
+
 if __name__ == "__main__":
     build(verbose=True)

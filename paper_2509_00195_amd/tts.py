@@ -16,7 +16,9 @@ from typing import Optional
 
 import numpy as np
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtts.so")
+# TTS_LIBRARY names another build of the same library (the sanitized CPU-test
+# build); by default the one built in this package's directory.
+LIB_PATH = os.environ.get("TTS_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtts.so")
 
 TTS_OK = 0
 TTS_ERR_INVALID_ARG = -1
