@@ -48,15 +48,19 @@ def parse():
     ap.add_argument("--warmup", type=int, default=56)
     ap.add_argument("--config", default="7b64")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--layers", type=int, default=28)
+    ap.add_argument("--layers", type=int, default=28,
+                    help="independent layer pools to rotate over (raised until they hold twice the 256 MB cache)")
     ap.add_argument("--variant", choices=["prefix", "paged"], default="prefix")
     ap.add_argument("--graph", action="store_true", help="replay the steps from a captured HIP graph")
     ap.add_argument("--q-len", type=int, default=1,
                     help="verification: every beam's last Q tokens are causal queries (prefix variant only; "
                          "value is then query tokens/s)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
-    ap.add_argument("--check", action="store_true", help="compare layer 0 against the oracle")
+    ap.add_argument("--cpu-seconds", type=float, default=16.0,
+                    help="host time for the oracle leg, split between one thread and all threads")
+    ap.add_argument("--no-check", action="store_true",
+                    help="skip comparing the call on layer 0 with the oracle (on by default; the oracle output "
+                         "of the cpu_baseline leg is reused)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after the timed region, stream this many MiB device-to-device three times with a plain "
                          "elementwise copy (dst = ~src; counter calibration runs)")
@@ -94,28 +98,79 @@ def make_layers(wl, x, layers, seed):
     return pools
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:  # pragma: no cover
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wl, budget_s):
-    """The oracle, as is, on the same batch: whole layer calls until the budget is used."""
+    """The oracle, as is, on the same batch: whole layer calls, first on one BLAS thread, then on all of them,
+    about half the budget each. Returns the record and the oracle's output of the first call."""
+    from threadpoolctl import threadpool_info, threadpool_limits
+
     from oracle.attention import oracle_attn_workload
 
-    try:
-        from threadpoolctl import threadpool_info
+    info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+    threads = max([i.get("num_threads", 1) for i in info] + [1])
+    blas = ", ".join(f"{i.get('internal_api')} {i.get('version')} ({i.get('threading_layer')})" for i in info) or "none"
 
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    def run(limit, budget):
+        n, first = 0, None
+        with threadpool_limits(limits=limit, user_api="blas"):
+            t0 = time.perf_counter()
+            while True:
+                out = oracle_attn_workload(wl)
+                if first is None:
+                    first = out
+                n += 1
+                el = time.perf_counter() - t0
+                if el >= budget or n >= 64:
+                    break
+        return n, el, first
+
+    n1, el1, ref = run(1, 0.5 * budget_s)
+    na, ela, _ = run(threads, 0.5 * budget_s)
+    rec = {"value": wl.num_seqs / (ela / na), "unit": "beam-tokens/s", "cores": int(threads), "kind": "oracle",
+           "value_1_thread": wl.num_seqs / (el1 / n1),
+           "host": {"os_cpu_count": os.cpu_count(), "cpu_model": _cpu_model(), "blas": blas},
+           "sample": f"{wl.name} batch ({wl.num_seqs} beams, all heads), whole layer calls, numpy fp32 oracle: "
+                     f"{n1} calls in {el1:.1f} s on 1 BLAS thread, {na} calls in {ela:.1f} s on {threads}"}
+    return rec, ref
+
+
+def meta_timings(wl, desc, reps=5):
+    """Host cost of the metadata (median of warm runs, ms): the trie, segments and beam order alone; the same
+    plus the work plan (host only, no allocation); and the full build with the device upload."""
+    from paper_2509_00195_amd import tts as T
+
+    def med(fn):
+        fn()
+        ts = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            fn()
+            ts.append((time.perf_counter() - t0) * 1e3)
+        return float(np.median(ts))
+
+    ncu = 256
+    try:
+        import torch
+
+        ncu = torch.cuda.get_device_properties(0).multi_processor_count
     except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
-    n = 0
-    t0 = time.perf_counter()
-    while True:
-        oracle_attn_workload(wl)
-        n += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s or n >= 64:
-            break
-    per = el / n
-    return {"value": wl.num_seqs / per, "unit": "beam-tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{n} full layer calls of the {wl.name} batch ({wl.num_seqs} beams, all heads) "
-                      f"in {el:.1f} s on the host, numpy fp32 ({threads} BLAS threads)"}
+        pass
+    args = (wl.req_seq_offsets, wl.block_tables, wl.seq_lens, wl.shape.block_size, wl.num_blocks)
+    return {
+        "host_trie_ms": med(lambda: T.tts_build_prefix_meta(*args)),
+        "host_trie_and_plan_ms": med(lambda: T.tts_plan_units_host(*args, desc, ncu)),
+        "build_with_upload_ms": med(lambda: T.tts_build_prefix_meta(*args, desc=desc)),
+    }
 
 
 COPY_KERNEL = "bitwise_not"  # the calibration copy: dst = ~src, one read and one write per byte
@@ -197,6 +252,7 @@ def main():
     t0 = time.perf_counter()
     pref = PrefixAttention(x, wl.req_seq_offsets, wl.block_tables, wl.seq_lens, wl.num_blocks, stream=stream)
     meta_ms = (time.perf_counter() - t0) * 1e3
+    meta_warm = meta_timings(wl, pref.desc) if args.q_len <= 1 else None
     view = pref.meta.export()
     units, slots = pref.meta.stats()
     eb = {"f32": 4, "bf16": 2, "fp8": 1}[sh.kv_dtype]
@@ -207,7 +263,9 @@ def main():
     logical_kv = logical_tokens * sh.num_kv_heads * sh.head_dim * 2 * eb
     paged = PagedAttention(x, wl.max_seq_len, wl.num_blocks)
 
-    pools = make_layers(wl, x, args.layers, args.seed)
+    pool_bytes = sum(t.numel() * t.element_size() for t in (x.k_cache, x.v_cache))
+    layers = max(args.layers, min(512, -(-2 * 256 * 2 ** 20 // max(pool_bytes, 1))))
+    pools = make_layers(wl, x, layers, args.seed)
     out = pref.out
     qlen = max(1, args.q_len)
     if qlen > 1:
@@ -226,6 +284,11 @@ def main():
     tabs, lens = x.block_tables, x.seq_lens
     maxb = int(tabs.shape[1])
 
+    # One rotation for every phase below: step i uses pool i mod L, and every
+    # phase continues from the last index, so a pool comes back only after
+    # the other L - 1 (at least twice the 256 MB cache of traffic).
+    rot = [0]
+
     def step(i, partials_only=False):
         q, k, v, ks, vs = pools[i % len(pools)]
         if qlen > 1:
@@ -239,25 +302,28 @@ def main():
             T.tts_paged_decode_attn(paged.desc, wl.num_seqs, q, k, v, ks, vs, tabs, maxb, lens, wl.max_seq_len,
                                     wl.num_blocks, out, paged.ws, paged.ws_bytes, stream)
 
-    check = None
-    if args.check and qlen == 1:
-        from oracle.attention import oracle_attn_workload
-
+    # Layer 0's output, for the comparison with the oracle (layer 0 holds the
+    # generator's inputs, the ones the oracle sees).
+    out0 = None
+    if not args.no_check and qlen == 1:
         step(0)
         torch.cuda.synchronize()
-        ref = oracle_attn_workload(wl)
-        check = float(np.max(np.abs(out.cpu().numpy() - ref)))
+        out0 = out.cpu().numpy().copy()
+    rot[0] = 1
 
-    for i in range(args.warmup):
-        step(i)
+    def steps(n, partials_only=False):
+        for _ in range(n):
+            step(rot[0], partials_only)
+            rot[0] += 1
+
+    steps(args.warmup)
     torch.cuda.synchronize()
 
     graph = None
     if args.graph:
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph, stream=stream):
-            for i in range(len(pools)):
-                step(i)
+            steps(len(pools))
         graph.replay()
         torch.cuda.synchronize()
 
@@ -275,11 +341,11 @@ def main():
     if graph is not None:
         reps = max(1, args.steps // len(pools))
         ms = timed(lambda n: [graph.replay() for _ in range(n)], reps)
-        steps = reps * len(pools)
+        nsteps = reps * len(pools)
     else:
-        ms = timed(lambda n: [step(i) for i in range(n)], args.steps)
-        steps = args.steps
-    ms_per_step = ms / steps
+        ms = timed(steps, args.steps)
+        nsteps = args.steps
+    ms_per_step = ms / nsteps
     value = wl.num_seqs * qlen / (ms_per_step * 1e-3)
 
     # For reference: the same calls replayed from one captured HIP graph per
@@ -289,8 +355,7 @@ def main():
     if graph is None:
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=stream):
-            for i in range(len(pools)):
-                step(i)
+            steps(len(pools))
         g.replay()
         reps = max(1, args.steps // len(pools))
         graph_call_us = timed(lambda n: [g.replay() for _ in range(n)], reps) * 1e3 / (reps * len(pools))
@@ -299,7 +364,7 @@ def main():
     # The dominant kernel alone (the attention work units of each call), same
     # rotation, events on the stream it runs on.
     if args.variant == "prefix":
-        kms = timed(lambda n: [step(i, partials_only=True) for i in range(n)], args.steps) / args.steps
+        kms = timed(lambda n: steps(n, partials_only=True), args.steps) / args.steps
     else:
         kms = ms_per_step
     kv_bytes = unique_kv if args.variant == "prefix" else logical_kv
@@ -358,7 +423,7 @@ def main():
         "value": value,
         "unit": "beam-tokens/s" if qlen == 1 else "query-tokens/s",
         "n_gpus": 1,
-        "steps": steps,
+        "steps": nsteps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
@@ -373,6 +438,7 @@ def main():
             "kv_dtype": sh.kv_dtype,
             "beams": wl.num_seqs,
             "layers_rotated": len(pools),
+            "layer_pool_bytes": int(pool_bytes),
             "graph_replay": bool(args.graph),
             "graph_call_us": graph_call_us,
             "q_len": qlen,
@@ -389,8 +455,9 @@ def main():
             "per_28_layer_step_beam_tokens_per_s": value / 28.0,
             "work_units": units,
             "partial_slots": slots,
-            "meta_build_ms": meta_ms,
-            "max_abs_err_vs_oracle": check,
+            "meta_first_build_ms": meta_ms,
+            "meta_warm_ms": meta_warm,
+            "max_abs_err_vs_oracle": None,
         },
         "roofline": {
             "bound": "hbm",
@@ -401,6 +468,7 @@ def main():
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": traffic,
+            "frac_per_call": kv_bytes / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
         },
     }
     if args.copy_mib > 0:
@@ -409,9 +477,15 @@ def main():
         for _ in range(3):
             torch.bitwise_not(src, out=dst)
         torch.cuda.synchronize()
+    ref = None
     if not args.no_cpu_baseline:
-        wl_cpu = make_workload(cfg, args.seed, poison=False)
-        rec["cpu_baseline"] = cpu_baseline(wl_cpu, args.cpu_seconds)
+        rec["cpu_baseline"], ref = cpu_baseline(wl, args.cpu_seconds)
+    if out0 is not None:
+        if ref is None:
+            from oracle.attention import oracle_attn_workload
+
+            ref = oracle_attn_workload(wl)
+        rec["config"]["max_abs_err_vs_oracle"] = float(np.max(np.abs(out0.astype(np.float64) - ref)))
     print(json.dumps(rec), flush=True)
 
 
