@@ -142,6 +142,21 @@ tts_status tts_build_prefix_meta(int32_t num_reqs, const int32_t* req_seq_offset
                                  const int32_t* seq_lens, int32_t block_size, int32_t num_blocks,
                                  const tts_attn_desc* desc, hipStream_t stream, tts_prefix_meta** out);
 
+/* The metadata of a batch after a fork (Sec. 3.1, Alg. 1: survivors are
+ * duplicated, each iteration's schedule is fixed once, Sec. 4.2), built from
+ * the previous batch's handle: the trie, segments and beam order are built
+ * for the new tables as tts_build_prefix_meta builds them (bit for bit), and
+ * the work plan starts from prev's target unit cost, scaled by the change in
+ * total work, instead of searching for one (the search is most of a full
+ * build's host time). The desc is prev's. Arguments, errors and result as in
+ * tts_build_prefix_meta (the plan may differ from the one a full build
+ * picks; attention results agree to rounding). prev: built with a desc, not
+ * a verification metadata; it stays valid and owned by the caller. */
+tts_status tts_fork_prefix_meta(const tts_prefix_meta* prev, int32_t num_reqs, const int32_t* req_seq_offsets,
+                                int32_t num_seqs, const int32_t* block_tables, int32_t max_blocks_per_seq,
+                                const int32_t* seq_lens, int32_t block_size, int32_t num_blocks, hipStream_t stream,
+                                tts_prefix_meta** out);
+
 /* Free a handle (NULL is ignored). The device buffer is released with
  * hipFree, which waits for work still using it. */
 void tts_prefix_meta_destroy(tts_prefix_meta* m);
@@ -353,6 +368,27 @@ tts_status tts_fork_tables(int32_t num_parents, const int32_t* parent_tables, in
                            const int32_t* child_parent, const int32_t* child_lens, const int32_t* free_ids,
                            int32_t num_free, int32_t* child_tables, int32_t* copies, int32_t* num_copies,
                            int32_t* num_free_used);
+
+/* Host: lengths of duplicated beams after speculation (Sec. 4.1, Alg. 1
+ * DuplicateThenTruncate: only the duplicates of a speculated beam lose
+ * speculative tokens, the original stays whole; the truncation is drawn from
+ * a normal distribution with mean R, the truncation ratio). Children are
+ * listed as for tts_fork_tables (child_parent[c] in [0, num_parents)); the
+ * first child of each parent is its original and keeps parent_lens[p]
+ * tokens; every later child of p keeps the parent's first
+ * parent_lens[p] - parent_spec[p] tokens plus
+ * floor(clip(ratio + sigma z[c], 0, 1) * parent_spec[p] + 0.5) of its
+ * parent_spec[p] speculative ones (the product sigma z[c] and the one with
+ * parent_spec rounded to double before the sums). z: one standard-normal
+ * draw per child (the caller's generator; entries of originals unused).
+ * The paper leaves the spread open; this build's default reading is
+ * sigma = 0.1. Writes child_lens[num_children] for tts_fork_tables.
+ * Errors (before anything is written): TTS_ERR_OUT_OF_RANGE for a bad parent,
+ * TTS_ERR_INVALID_ARG for parent_spec outside [0, parent length], a
+ * non-finite ratio or z, or sigma < 0. */
+tts_status tts_truncated_lengths(int32_t num_children, const int32_t* child_parent, const int32_t* parent_lens,
+                                 const int32_t* parent_spec, int32_t num_parents, double ratio, double sigma,
+                                 const double* z, int32_t* child_lens);
 
 /* ---- Roofline-guided KV allocation (Sec. 4.3) -------------------------------
  *

@@ -16,8 +16,10 @@ slow and written to be checked by eye against its definitions:
 * ``fp8.e4m3_table`` -- the 256 OCP E4M3FN code values from the bit formula.
 * ``kv_ops`` -- the KV-cache steps around decode: E4M3 encoding by nearest
   table value, appending each beam's token (with the fp8 block-scale rule),
-  block copies, and the block tables of duplicated beams
-  (DuplicateThenTruncate, Sec. 3.1 and Alg. 1).
+  block copies, the block tables of duplicated beams
+  (DuplicateThenTruncate, Sec. 3.1 and Alg. 1) and the lengths the
+  duplicates keep after speculation (truncation drawn around the ratio R,
+  Sec. 4.1).
 * ``schedule`` -- dynamic prefix-aware scheduling (Sec. 4.2): the greedy
   shared-prefix order, budgeted batches and the eviction cost.
 * ``kv_alloc`` -- roofline-guided KV allocation (Sec. 4.3): the modelled
@@ -37,5 +39,5 @@ routine or hand-derived golden fixtures.
 
 from .attention import decode_bf16, oracle_attn, oracle_attn_row, oracle_verify_attn  # noqa: F401
 from .fp8 import e4m3_table  # noqa: F401
-from .kv_ops import append_kv, copy_blocks, e4m3_encode, fork_tables  # noqa: F401
+from .kv_ops import append_kv, copy_blocks, e4m3_encode, fork_tables, truncated_lengths  # noqa: F401
 from .prefix_meta import oracle_coverage, oracle_prefix_meta  # noqa: F401

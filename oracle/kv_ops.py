@@ -16,6 +16,13 @@ full blocks and a private copy of the partially filled block it keeps
   it), every step in fp32 as the definition orders it.
 * ``copy_blocks`` and ``fork_tables``: whole-block copies, and the
   children's tables (shared full blocks, one copied partial block each).
+* ``truncated_lengths``: how many tokens each child keeps (Sec. 4.1,
+  Alg. 1): an original keeps all of its parent's; a duplicate of a parent
+  that speculated keeps the fraction clip(R + sigma z, 0, 1) of the parent's
+  speculative tokens, drawn from a normal distribution with mean R (the
+  truncation ratio), rounded half up. The paper gives no spread and no
+  rounding: sigma (default reading 0.1) and the rounding are this build's
+  readings; the standard-normal draws z are inputs.
 
 The paper fixes none of the numeric policy: the fp8 scale rule is this
 build's reading (one fp32 scale per block and tensor, as the workload
@@ -169,3 +176,25 @@ def fork_tables(parent_tables, parent_lens, block_size, child_parent, child_lens
             tables[c, full] = dst
             copies.append((int(parent_tables[par, full]), dst))
     return tables, np.asarray(copies, dtype=np.int32).reshape(-1, 2), used
+
+
+def truncated_lengths(child_parent, parent_lens, parent_spec, ratio, sigma, z):
+    """Tokens kept by each child: the first child of a parent (its original) keeps the parent's
+    length; every later one keeps the non-speculative prefix plus
+    floor(clip(ratio + sigma * z[c], 0, 1) * spec + 1/2) of the parent's spec speculative tokens
+    (Python floats: each product and sum rounded to double in that order)."""
+    out = []
+    seen = set()
+    for c, par in enumerate(child_parent):
+        par = int(par)
+        length, spec = int(parent_lens[par]), int(parent_spec[par])
+        assert 0 <= spec <= length
+        if par not in seen:
+            seen.add(par)
+            out.append(length)
+            continue
+        f = float(ratio) + float(sigma) * float(z[c])
+        f = min(max(f, 0.0), 1.0)
+        kept = min(spec, int(np.floor(f * float(spec) + 0.5)))
+        out.append(length - spec + kept)
+    return np.asarray(out, dtype=np.int32)

@@ -16,10 +16,12 @@ from .tts import (  # noqa: F401
     tts_build_prefix_meta,
     tts_build_verify_meta,
     tts_copy_blocks,
+    tts_fork_prefix_meta,
     tts_fork_tables,
     tts_kv_alloc_search,
     tts_kv_alloc_time,
     tts_prefix_schedule,
+    tts_truncated_lengths,
     tts_prefix_verify_attn,
     tts_paged_decode_attn,
     tts_paged_decode_workspace_size,

@@ -39,6 +39,15 @@ hipError_t launch_copy_blocks(const int32_t* pairs, int num_pairs, void* k_cache
                               float* v_scale, int64_t blk_bytes, int num_blocks, hipStream_t stream);
 }  // namespace tts
 
+namespace tts {
+// A product the compiler may not fuse with a following addition (an FMA
+// would round once where the oracle rounds twice).
+double mul_unfused(double a, double b) {
+  volatile double r = a * b;
+  return r;
+}
+}  // namespace tts
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -117,7 +126,8 @@ const char* tts_last_error(void) { return g_last_error.c_str(); }
 static tts_status build_meta_impl(int32_t num_reqs, const int32_t* req_seq_offsets, int32_t num_seqs,
                                   const int32_t* block_tables, int32_t max_blocks_per_seq, const int32_t* seq_lens,
                                   int32_t block_size, int32_t num_blocks, const tts_attn_desc* desc,
-                                  hipStream_t stream, int32_t q_len, tts_prefix_meta** out) {
+                                  hipStream_t stream, int32_t q_len, tts_prefix_meta** out,
+                                  const tts::WorkPlan* warm = nullptr) {
   if (!out) return fail(TTS_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   if (desc) {
@@ -161,7 +171,7 @@ static tts_status build_meta_impl(int32_t num_reqs, const int32_t* req_seq_offse
     }
     try {
       tts::build_work_plan(m->host, {desc->num_q_heads, desc->num_kv_heads, desc->head_dim, kv_bytes(desc), ncu},
-                           &m->plan);
+                           &m->plan, warm);
     } catch (const std::bad_alloc&) {
       delete m;
       return fail(TTS_ERR_NOMEM, "out of host memory");
@@ -229,6 +239,54 @@ tts_status tts_build_verify_meta(int32_t num_reqs, const int32_t* req_seq_offset
     }
   return build_meta_impl(num_reqs, voff.data(), static_cast<int32_t>(vs), vtab.data(), max_blocks_per_seq,
                          vlen.data(), block_size, num_blocks, desc, stream, q_len, out);
+}
+
+tts_status tts_fork_prefix_meta(const tts_prefix_meta* prev, int32_t num_reqs, const int32_t* req_seq_offsets,
+                                int32_t num_seqs, const int32_t* block_tables, int32_t max_blocks_per_seq,
+                                const int32_t* seq_lens, int32_t block_size, int32_t num_blocks, hipStream_t stream,
+                                tts_prefix_meta** out) {
+  if (out) *out = nullptr;
+  if (!prev) return fail(TTS_ERR_INVALID_ARG, "prev is NULL");
+  if (!prev->has_plan) return fail(TTS_ERR_INVALID_ARG, "prev was built without a desc");
+  if (prev->q_len != 1) return fail(TTS_ERR_INVALID_ARG, "prev is a verification metadata");
+  return build_meta_impl(num_reqs, req_seq_offsets, num_seqs, block_tables, max_blocks_per_seq, seq_lens, block_size,
+                         num_blocks, &prev->desc, stream, 1, out, &prev->plan);
+}
+
+tts_status tts_truncated_lengths(int32_t num_children, const int32_t* child_parent, const int32_t* parent_lens,
+                                 const int32_t* parent_spec, int32_t num_parents, double ratio, double sigma,
+                                 const double* z, int32_t* child_lens) {
+  if (num_children < 0 || num_parents < 0) return fail(TTS_ERR_INVALID_ARG, "negative count");
+  if (num_children > 0 && (!child_parent || !z || !child_lens || !parent_lens || !parent_spec))
+    return fail(TTS_ERR_INVALID_ARG, "NULL host array");
+  if (!std::isfinite(ratio) || !std::isfinite(sigma) || sigma < 0)
+    return fail(TTS_ERR_INVALID_ARG, "ratio must be finite and sigma finite and >= 0");
+  for (int32_t c = 0; c < num_children; ++c) {
+    const int32_t p = child_parent[c];
+    if (p < 0 || p >= num_parents) return fail(TTS_ERR_OUT_OF_RANGE, "child_parent out of range");
+    if (parent_spec[p] < 0 || parent_spec[p] > parent_lens[p])
+      return fail(TTS_ERR_INVALID_ARG, "parent_spec must lie in [0, parent length]");
+    if (!std::isfinite(z[c])) return fail(TTS_ERR_INVALID_ARG, "z is not finite");
+  }
+  std::vector<char> seen(static_cast<size_t>(num_parents), 0);
+  for (int32_t c = 0; c < num_children; ++c) {
+    const int32_t p = child_parent[c];
+    if (!seen[p]) {  // the original keeps every token
+      seen[p] = 1;
+      child_lens[c] = parent_lens[p];
+      continue;
+    }
+    // A duplicate keeps the fraction clip(ratio + sigma z, 0, 1) of its
+    // parent's speculative tokens, rounded half up (two roundings: the
+    // product, then the sum, never fused, as the oracle computes it).
+    const double dz = tts::mul_unfused(sigma, z[c]);
+    double f = ratio + dz;
+    f = f < 0.0 ? 0.0 : (f > 1.0 ? 1.0 : f);
+    const int32_t spec = parent_spec[p];
+    const int32_t kept = static_cast<int32_t>(std::floor(tts::mul_unfused(f, static_cast<double>(spec)) + 0.5));
+    child_lens[c] = parent_lens[p] - spec + (kept > spec ? spec : kept);
+  }
+  return ok();
 }
 
 void tts_prefix_meta_destroy(tts_prefix_meta* m) {

@@ -71,6 +71,11 @@ struct WorkPlan {
   bool two_windows = false;       // some record has a second entry window
   int64_t num_units = 0;          // records with work
   int64_t num_slots = 0;          // slot_rows.size()
+  // The planner's choices, for a warm re-plan of the next batch: the target
+  // unit cost (us), the modelled work per workgroup it was chosen for, and
+  // whether the units were chained (more units than workgroups).
+  double target_us = 0, work_us = 0;
+  bool chained = false;
 };
 
 struct PlanShape {
@@ -78,6 +83,9 @@ struct PlanShape {
   int32_t num_bins;  // persistent workgroups (one per compute unit)
 };
 
-void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan);
+// warm: a plan of an earlier batch of the same shape (e.g. before a fork);
+// when given, its target unit cost, scaled by the change in work, is used
+// instead of searching one (the search is most of a plan's host time).
+void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, const WorkPlan* warm = nullptr);
 
 }  // namespace tts

@@ -111,7 +111,7 @@ void touched_beams(const Tmpl& t, int32_t g, std::vector<char>* out) {
 
 }  // namespace
 
-void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) {
+void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, const WorkPlan* warm) {
   WorkPlan& P = *plan;
   P = WorkPlan();
   const int32_t S = m.num_seqs;
@@ -424,64 +424,82 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan) 
     make_templates(T, tm, ngroups);
     return static_cast<int32_t>(tm.size());
   };
-  // Upper bound of the search: a few times the average work per unit, raised
-  // while the units do not fit (one entry of many rows can cost more than
-  // that bound by its row term alone; without the raise such a batch would
-  // fall to the chained plans, with one tiny unit per entry).
-  double hi = kUnitFixedUs + 4.0 * work + 1.0;
-  for (int it = 0; it < 6 && units_at(hi) > fit_units; ++it) hi *= 2.0;
-  if (units_at(hi) <= fit_units) {
-    double lo = kUnitFixedUs;
-    for (int it = 0; it < 24; ++it) {
-      const double mid = 0.5 * (lo + hi);
-      if (units_at(mid) <= fit_units)
-        hi = mid;
-      else
-        lo = mid;
-    }
-    // Longer units mean fewer partial states per beam, so a cheaper merge:
-    // take the target (the smallest one's variable part scaled up) with the
-    // least modelled attention plus merge time.
-    std::vector<char> touched;
-    auto most_slots = [&](const std::vector<Tmpl>& t) {
-      std::vector<int32_t> cnt(S, 0);
-      for (const Tmpl& x : t) {
-        touched_beams(x, g, &touched);
-        for (int32_t i = 0; i < x.hi - x.lo; ++i)
-          if (touched[i]) ++cnt[m.perm[x.lo + i]];
-      }
-      return S > 0 ? *std::max_element(cnt.begin(), cnt.end()) : 0;
-    };
-    const double t_min = hi;
-    double best_T = t_min, best_est = -1;
-    for (double f : {1.0, 1.5, 2.0, 3.0, 4.0, 6.0}) {
-      const double T = kUnitFixedUs + f * (t_min - kUnitFixedUs);
-      if (units_at(T) > fit_units) continue;
-      double ms = 0;
-      for (const Tmpl& x : tm) ms = std::max(ms, x.cost);
-      const int32_t slots = most_slots(tm);
-      const double est = ms + kMergeFixedUs + kMergeBatchUs * ((slots + kMergeBatch - 1) / kMergeBatch);
-      if (best_est < 0 || est < best_est) {
-        best_est = est;
-        best_T = T;
-      }
-    }
-    units_at(best_T);
+  P.work_us = work;
+  if (warm && warm->target_us > 0 && warm->work_us > 0) {
+    // Warm re-plan: the earlier target, scaled with the work, raised while
+    // its units outnumber the workgroups (unless that plan was chained);
+    // one placement, no search.
+    double T = kUnitFixedUs + (warm->target_us - kUnitFixedUs) * (work / warm->work_us);
+    T = std::max(T, kUnitFixedUs + 1e-3);
+    if (!warm->chained)
+      for (int it = 0; it < 12 && units_at(T) > fit_units; ++it) T = kUnitFixedUs + 1.15 * (T - kUnitFixedUs);
+    units_at(T);
     place(tm, ngroups, bins);
+    P.target_us = T;
+    P.chained = warm->chained;
   } else {
-    std::vector<Tmpl> cand;
-    std::vector<std::vector<Work>> cbins;
-    double best = -1;
-    for (double f : {0.35, 0.5, 0.65, 0.8, 1.0, 1.2, 1.45, 1.75, 2.1, 2.5, 3.0, 4.0}) {
-      int32_t cg = 0;
-      make_templates(kUnitFixedUs + f * work, cand, cg);
-      const double ms = place(cand, cg, cbins);
-      if (best < 0 || ms < best) {
-        best = ms;
-        tm.swap(cand);
-        bins.swap(cbins);
-        ngroups = cg;
+    // Upper bound of the search: a few times the average work per unit,
+    // raised while the units do not fit (one entry of many rows can cost
+    // more than that bound by its row term alone; without the raise such a
+    // batch would fall to the chained plans, with one tiny unit per entry).
+    double hi = kUnitFixedUs + 4.0 * work + 1.0;
+    for (int it = 0; it < 6 && units_at(hi) > fit_units; ++it) hi *= 2.0;
+    if (units_at(hi) <= fit_units) {
+      double lo = kUnitFixedUs;
+      for (int it = 0; it < 24; ++it) {
+        const double mid = 0.5 * (lo + hi);
+        if (units_at(mid) <= fit_units)
+          hi = mid;
+        else
+          lo = mid;
       }
+      // Longer units mean fewer partial states per beam, so a cheaper merge:
+      // take the target (the smallest one's variable part scaled up) with the
+      // least modelled attention plus merge time.
+      std::vector<char> touched;
+      auto most_slots = [&](const std::vector<Tmpl>& t) {
+        std::vector<int32_t> cnt(S, 0);
+        for (const Tmpl& x : t) {
+          touched_beams(x, g, &touched);
+          for (int32_t i = 0; i < x.hi - x.lo; ++i)
+            if (touched[i]) ++cnt[m.perm[x.lo + i]];
+        }
+        return S > 0 ? *std::max_element(cnt.begin(), cnt.end()) : 0;
+      };
+      const double t_min = hi;
+      double best_T = t_min, best_est = -1;
+      for (double f : {1.0, 1.5, 2.0, 3.0, 4.0, 6.0}) {
+        const double T = kUnitFixedUs + f * (t_min - kUnitFixedUs);
+        if (units_at(T) > fit_units) continue;
+        double ms = 0;
+        for (const Tmpl& x : tm) ms = std::max(ms, x.cost);
+        const int32_t slots = most_slots(tm);
+        const double est = ms + kMergeFixedUs + kMergeBatchUs * ((slots + kMergeBatch - 1) / kMergeBatch);
+        if (best_est < 0 || est < best_est) {
+          best_est = est;
+          best_T = T;
+        }
+      }
+      units_at(best_T);
+      place(tm, ngroups, bins);
+      P.target_us = best_T;
+    } else {
+      std::vector<Tmpl> cand;
+      std::vector<std::vector<Work>> cbins;
+      double best = -1;
+      for (double f : {0.35, 0.5, 0.65, 0.8, 1.0, 1.2, 1.45, 1.75, 2.1, 2.5, 3.0, 4.0}) {
+        int32_t cg = 0;
+        make_templates(kUnitFixedUs + f * work, cand, cg);
+        const double ms = place(cand, cg, cbins);
+        if (best < 0 || ms < best) {
+          best = ms;
+          tm.swap(cand);
+          bins.swap(cbins);
+          ngroups = cg;
+          P.target_us = kUnitFixedUs + f * work;
+        }
+      }
+      P.chained = true;
     }
   }
 

@@ -40,7 +40,7 @@ EXPORTED = [
     "tts_prefix_decode_partials",
     "tts_prefix_decode_merge", "tts_append_kv", "tts_copy_blocks", "tts_fork_tables", "tts_kv_alloc_time",
     "tts_kv_alloc_search", "tts_prefix_schedule", "tts_build_verify_meta", "tts_prefix_verify_attn",
-    "tts_last_error",
+    "tts_last_error", "tts_fork_prefix_meta", "tts_truncated_lengths",
 ]
 
 
@@ -107,6 +107,10 @@ def load() -> C.CDLL:
     lib.tts_build_verify_meta.restype = C.c_int
     lib.tts_build_verify_meta.argtypes = [I32, pi32, I32, pi32, I32, pi32, I32, I32, I32, P(tts_attn_desc), VP,
                                           P(VP)]
+    lib.tts_fork_prefix_meta.restype = C.c_int
+    lib.tts_fork_prefix_meta.argtypes = [VP, I32, pi32, I32, pi32, I32, pi32, I32, I32, VP, P(VP)]
+    lib.tts_truncated_lengths.restype = C.c_int
+    lib.tts_truncated_lengths.argtypes = [I32, pi32, pi32, pi32, I32, C.c_double, C.c_double, P(C.c_double), pi32]
     lib.tts_prefix_meta_destroy.restype = None
     lib.tts_prefix_meta_destroy.argtypes = [VP]
     lib.tts_prefix_meta_export.restype = C.c_int
@@ -238,6 +242,36 @@ def tts_build_prefix_meta(req_seq_offsets, block_tables, seq_lens, block_size: i
                                      block_size, num_blocks, C.byref(desc) if desc is not None else None,
                                      _stream(stream) if desc is not None else None, C.byref(h)))
     return PrefixMeta(h.value, desc)
+
+
+def tts_fork_prefix_meta(prev: PrefixMeta, req_seq_offsets, block_tables, seq_lens, block_size: int, num_blocks: int,
+                         stream=None) -> PrefixMeta:
+    lib = load()
+    offs = _host_i32(req_seq_offsets)
+    tables = _host_i32(block_tables)
+    lens = _host_i32(seq_lens)
+    s = lens.shape[0]
+    maxb = tables.shape[1] if tables.ndim == 2 else 0
+    h = C.c_void_p()
+    _check(lib.tts_fork_prefix_meta(prev.handle, offs.shape[0] - 1, _as_i32p(offs), s, _as_i32p(tables), maxb,
+                                    _as_i32p(lens), block_size, num_blocks, _stream(stream), C.byref(h)))
+    return PrefixMeta(h.value, prev.desc)
+
+
+def tts_truncated_lengths(child_parent, parent_lens, parent_spec, ratio: float, sigma: float, z) -> np.ndarray:
+    """Lengths of the children of a duplication step (originals whole, duplicates truncated)."""
+    lib = load()
+    cp = _host_i32(child_parent)
+    pl = _host_i32(parent_lens)
+    ps = _host_i32(parent_spec)
+    zz = np.ascontiguousarray(z, dtype=np.float64)
+    n = cp.shape[0]
+    if zz.shape[0] != n or ps.shape[0] != pl.shape[0]:
+        raise ValueError("z needs one draw per child and parent_spec one entry per parent")
+    out = np.zeros(n, np.int32)
+    _check(lib.tts_truncated_lengths(n, _as_i32p(cp), _as_i32p(pl), _as_i32p(ps), pl.shape[0], float(ratio),
+                                     float(sigma), zz.ctypes.data_as(C.POINTER(C.c_double)), _as_i32p(out)))
+    return out
 
 
 def tts_build_verify_meta(req_seq_offsets, block_tables, seq_lens, q_len: int, block_size: int, num_blocks: int,

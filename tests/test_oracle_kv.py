@@ -169,3 +169,73 @@ def test_host_fork_errors():
         tts_fork_tables(pt, [20], 16, [0], [21], [9])  # longer than the parent
     with pytest.raises(TTSError):
         tts_fork_tables(pt, [20], 16, [0, 0], [5, 6], [9])  # not enough free blocks
+
+
+# ---- truncation of duplicated beams (Sec. 4.1, Alg. 1 DuplicateThenTruncate) -------------
+
+def test_truncated_lengths_hand_derived():
+    """Parents of lengths 100 and 50 with 20 and 0 speculative tokens; children 0, 0, 0, 1, 1.
+    The first child of each parent is its original: 100 and 50. With R = 0.85, sigma = 0.1:
+    z = 1 -> 0.95 * 20 = 19 kept -> 99; z = -2 -> 0.65 * 20 = 13 -> 93; parent 1 has nothing
+    speculative -> 50 whatever z."""
+    from oracle.kv_ops import truncated_lengths
+
+    cp = [0, 0, 0, 1, 1]
+    got = truncated_lengths(cp, [100, 50], [20, 0], 0.85, 0.1, [5.0, 1.0, -2.0, 0.0, -3.0])
+    assert got.tolist() == [100, 99, 93, 50, 50]
+    # clipping: z = 3 -> 1.15 -> 1 (all 20 kept); z = -9 -> -0.05 -> 0 (none)
+    assert truncated_lengths([0, 0, 0], [100], [20], 0.85, 0.1, [0.0, 3.0, -9.0]).tolist() == [100, 100, 80]
+    # R = 1 with no spread keeps everything; R = 0 drops every speculative token
+    assert truncated_lengths([0, 0], [30], [7], 1.0, 0.0, [0.0, 0.5]).tolist() == [30, 30]
+    assert truncated_lengths([0, 0], [30], [7], 0.0, 0.0, [0.0, 0.5]).tolist() == [30, 23]
+    # z = 0 rounds R * spec half up: 0.5 * 7 = 3.5 -> 4
+    assert truncated_lengths([0, 0], [30], [7], 0.5, 0.1, [0.0, 0.0]).tolist() == [30, 27]
+
+
+def test_truncated_fraction_follows_the_clipped_normal():
+    """Over many duplicates the kept fraction averages E[clip(N(R, sigma^2), 0, 1)], computed by
+    numerical integration of the normal density (scipy), within four standard errors."""
+    from scipy import integrate, stats
+
+    from oracle.kv_ops import truncated_lengths
+
+    rng = np.random.default_rng(11)
+    n, spec = 20000, 1000
+    for ratio, sigma in [(0.85, 0.1), (0.5, 0.3)]:
+        z = rng.standard_normal(n + 1)
+        lens = truncated_lengths(np.zeros(n + 1, np.int32), [5000], [spec], ratio, sigma, z)[1:]
+        frac = (lens - (5000 - spec)) / spec
+        want = integrate.quad(lambda x: min(max(ratio + sigma * x, 0.0), 1.0) * stats.norm.pdf(x), -12, 12,
+                              points=[(0 - ratio) / sigma, (1 - ratio) / sigma])[0]
+        assert abs(frac.mean() - want) <= 4 * frac.std() / np.sqrt(n) + 0.5 / spec
+        assert frac.min() >= 0 and frac.max() <= 1
+
+
+def test_library_truncated_lengths_match_oracle():
+    from oracle.kv_ops import truncated_lengths
+    from paper_2509_00195_amd import tts_truncated_lengths
+
+    rng = np.random.default_rng(12)
+    for _ in range(200):
+        npar = int(rng.integers(1, 9))
+        plens = rng.integers(0, 300, npar).astype(np.int32)
+        pspec = np.array([rng.integers(0, L + 1) for L in plens], np.int32)
+        cp = np.sort(rng.integers(0, npar, int(rng.integers(1, 30)))).astype(np.int32)
+        ratio, sigma = float(rng.uniform(-0.2, 1.2)), float(rng.choice([0.0, 0.05, 0.1, 0.5]))
+        z = rng.standard_normal(len(cp))
+        z[rng.random(len(cp)) < 0.2] = 0.0  # exact halves
+        assert np.array_equal(tts_truncated_lengths(cp, plens, pspec, ratio, sigma, z),
+                              truncated_lengths(cp, plens, pspec, ratio, sigma, z))
+
+
+def test_library_truncated_lengths_errors():
+    from paper_2509_00195_amd import TTSError, tts_truncated_lengths
+
+    with pytest.raises(TTSError):
+        tts_truncated_lengths([0, 2], [10, 10], [1, 1], 0.85, 0.1, [0.0, 0.0])  # bad parent
+    with pytest.raises(TTSError):
+        tts_truncated_lengths([0, 0], [10], [11], 0.85, 0.1, [0.0, 0.0])  # more speculative than tokens
+    with pytest.raises(TTSError):
+        tts_truncated_lengths([0, 0], [10], [1], 0.85, -0.1, [0.0, 0.0])  # negative spread
+    with pytest.raises(TTSError):
+        tts_truncated_lengths([0, 0], [10], [1], 0.85, 0.1, [0.0, float("nan")])
