@@ -144,9 +144,11 @@ def cpu_baseline(wl, budget_s):
     return rec, ref
 
 
-def meta_timings(wl, desc, reps=5):
+def meta_timings(wl, desc, prev, reps=5):
     """Host cost of the metadata (median of warm runs, ms): the trie, segments and beam order alone; the same
-    plus the work plan (host only, no allocation); and the full build with the device upload."""
+    plus the work plan (host only, no allocation); the full build with the device upload; and the update after a
+    fork, re-planned warm from the previous metadata (tts_fork_prefix_meta; timed on the same tables, whose
+    sizes set its cost)."""
     from paper_2509_00195_amd import tts as T
 
     def med(fn):
@@ -170,6 +172,7 @@ def meta_timings(wl, desc, reps=5):
         "host_trie_ms": med(lambda: T.tts_build_prefix_meta(*args)),
         "host_trie_and_plan_ms": med(lambda: T.tts_plan_units_host(*args, desc, ncu)),
         "build_with_upload_ms": med(lambda: T.tts_build_prefix_meta(*args, desc=desc)),
+        "fork_update_ms": med(lambda: T.tts_fork_prefix_meta(prev, *args)),
     }
 
 
@@ -252,7 +255,7 @@ def main():
     t0 = time.perf_counter()
     pref = PrefixAttention(x, wl.req_seq_offsets, wl.block_tables, wl.seq_lens, wl.num_blocks, stream=stream)
     meta_ms = (time.perf_counter() - t0) * 1e3
-    meta_warm = meta_timings(wl, pref.desc) if args.q_len <= 1 else None
+    meta_warm = meta_timings(wl, pref.desc, pref.meta) if args.q_len <= 1 else None
     view = pref.meta.export()
     units, slots = pref.meta.stats()
     eb = {"f32": 4, "bf16": 2, "fp8": 1}[sh.kv_dtype]

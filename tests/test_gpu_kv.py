@@ -13,15 +13,17 @@ import pytest
 import torch
 
 from oracle.attention import oracle_attn
-from oracle.kv_ops import append_kv, copy_blocks, fork_tables
+from oracle.kv_ops import append_kv, copy_blocks, fork_tables, truncated_lengths
 from paper_2509_00195_amd import (
     make_desc,
     tts_append_kv,
     tts_build_prefix_meta,
     tts_copy_blocks,
+    tts_fork_prefix_meta,
     tts_fork_tables,
     tts_prefix_decode_attn,
     tts_prefix_decode_workspace_size,
+    tts_truncated_lengths,
 )
 
 pytestmark = pytest.mark.gpu
@@ -134,9 +136,12 @@ def test_copy_blocks_bit_exact(kv):
 def test_beam_search_replay(kv):
     """A small search on both sides: every step appends one token per beam (a block is
     allocated when a beam crosses into a new one), every 12 steps half the beams survive and
-    are duplicated, each child keeping its parent's tokens minus a few speculative ones
-    (copy-on-write of the kept partial block). After every step: caches bit-exact and the
-    prefix-shared attention (metadata rebuilt) within tolerance of the oracle's."""
+    are duplicated: the last 0-5 tokens of each survivor count as speculative, its original
+    keeps them and its duplicate keeps a share drawn around R = 0.85 (tts_truncated_lengths
+    against the oracle's truncated_lengths, same draws), with copy-on-write of the kept
+    partial block. After every step: caches bit-exact; every 8 steps the prefix-shared
+    attention within tolerance of the oracle's, with the metadata both rebuilt in full and
+    re-planned warm from the previous step's (tts_fork_prefix_meta; same trie and order)."""
     rng = np.random.default_rng(7)
     hq, hkv, d, nb, maxb, s = 8, 2, 128, 160, 8, 8
     desc = make_desc(hq, hkv, d, kv_dtype=kv)
@@ -166,6 +171,7 @@ def test_beam_search_replay(kv):
     copy_blocks(k, v, ks, vs, copies)
     dt = _store_dtype(kv)
     ks0 = ks.copy() if ks is not None else None
+    prev_meta = None
     for step in range(40):
         # allocate the block a beam is about to enter
         for b in range(s):
@@ -180,7 +186,10 @@ def test_beam_search_replay(kv):
         if step % 12 == 11:
             surv = np.sort(rng.choice(s, s // 2, replace=False))
             cp = np.repeat(surv, 2).astype(np.int32)
-            cl = np.array([lens[p] - int(rng.integers(0, 4)) for p in cp], np.int32)
+            spec = np.minimum(rng.integers(0, 6, s), lens).astype(np.int32)
+            z = rng.standard_normal(len(cp))
+            cl = tts_truncated_lengths(cp, lens, spec, 0.85, 0.1, z)
+            assert np.array_equal(cl, truncated_lengths(cp, lens, spec, 0.85, 0.1, z))
             new_t, copies, used = tts_fork_tables(tables, lens, BS, cp, cl, np.array(free, np.int32))
             ot, oc, ou = fork_tables(tables, lens, BS, cp, cl, np.array(free, np.int32))
             assert np.array_equal(new_t, ot) and np.array_equal(copies, oc) and used == ou
@@ -198,16 +207,58 @@ def test_beam_search_replay(kv):
         if step % 8 == 7:
             q = _bf16_bits(rng.normal(0, 1, (s, hq, d)))
             offs = np.array([0, s], np.int32)
-            meta = tts_build_prefix_meta(offs, tables, lens, BS, nb, desc=desc)
-            ws_bytes = tts_prefix_decode_workspace_size(desc, meta)
-            ws = torch.zeros(max(ws_bytes, 1), dtype=torch.uint8, device=DEV)
-            out = torch.zeros((s, hq, d), dtype=torch.float32, device=DEV)
-            tts_prefix_decode_attn(desc, meta, _to_dev(q), dk, dv, dks, dvs, _to_dev(tables), maxb, _to_dev(lens),
-                                   nb, out, ws, ws_bytes)
+            metas = [tts_build_prefix_meta(offs, tables, lens, BS, nb, desc=desc)]
+            if prev_meta is not None:
+                metas.append(tts_fork_prefix_meta(prev_meta, offs, tables, lens, BS, nb))
+                full, warm = metas[0].export(), metas[1].export()
+                for key in ("perm", "seg_beam_begin", "seg_beam_end", "seg_nblocks", "tail_lblock"):
+                    assert np.array_equal(full[key], warm[key]), key
             ref = oracle_attn(q, k, v, ks, vs, tables, lens, num_q_heads=hq, num_kv_heads=hkv, block_size=BS,
                               q_dtype="bf16", kv_dtype=kv)
-            err = float(np.max(np.abs(out.cpu().numpy() - ref)))
-            regrow = int(np.sum(ks != ks0)) if ks is not None else 0
-            print(f"replay {kv} step {step}: err {err:.2e}, fp8 scales changed since the prompt: {regrow}",
-                  flush=True)
-            assert err <= TOL[kv]
+            for meta in metas:
+                ws_bytes = tts_prefix_decode_workspace_size(desc, meta)
+                ws = torch.zeros(max(ws_bytes, 1), dtype=torch.uint8, device=DEV)
+                out = torch.zeros((s, hq, d), dtype=torch.float32, device=DEV)
+                tts_prefix_decode_attn(desc, meta, _to_dev(q), dk, dv, dks, dvs, _to_dev(tables), maxb,
+                                       _to_dev(lens), nb, out, ws, ws_bytes)
+                err = float(np.max(np.abs(out.cpu().numpy() - ref)))
+                regrow = int(np.sum(ks != ks0)) if ks is not None else 0
+                print(f"replay {kv} step {step} ({'warm' if meta is not metas[0] else 'full'} plan): err "
+                      f"{err:.2e}, fp8 scales changed since the prompt: {regrow}", flush=True)
+                assert err <= TOL[kv]
+            prev_meta = metas[0]
+
+
+@pytest.mark.parametrize("name", ["7b64", "7b_straggler"])
+def test_fork_prefix_meta_at_config_scale(name):
+    """The metadata of the next search iteration re-planned warm from the current one's
+    (tts_fork_prefix_meta: seed 1's tree after seed 0's, same shape): the same trie, segments and
+    beam order as a full build, and attention within tolerance of the oracle."""
+    from oracle.attention import oracle_attn_workload
+    from paper_2509_00195_amd.runner import PrefixAttention
+    from tts_synth import make_workload
+    from tts_synth.device import to_device
+
+    prev_wl = make_workload(name, 0)
+    prev = PrefixAttention(to_device(prev_wl), prev_wl.req_seq_offsets, prev_wl.block_tables, prev_wl.seq_lens,
+                           prev_wl.num_blocks)
+    wl = make_workload(name, 1)
+    x = to_device(wl)
+    full = PrefixAttention(x, wl.req_seq_offsets, wl.block_tables, wl.seq_lens, wl.num_blocks)
+    warm = tts_fork_prefix_meta(prev.meta, wl.req_seq_offsets, wl.block_tables, wl.seq_lens, BS, wl.num_blocks)
+    ef, ew = full.meta.export(), warm.export()
+    for key in ("perm", "seg_req", "seg_parent", "seg_lblock_begin", "seg_nblocks", "seg_beam_begin", "seg_beam_end",
+                "tail_lblock"):
+        assert np.array_equal(ef[key], ew[key]), key
+    assert ef["unique_tokens"] == ew["unique_tokens"]
+    ws_bytes = tts_prefix_decode_workspace_size(full.desc, warm)
+    ws = torch.zeros(max(ws_bytes, 1), dtype=torch.uint8, device=DEV)
+    out = torch.full_like(full.out, float("nan"))
+    tts_prefix_decode_attn(full.desc, warm, x.q, x.k_cache, x.v_cache, x.k_scale, x.v_scale, x.block_tables,
+                           int(x.block_tables.shape[1]), x.seq_lens, wl.num_blocks, out, ws, ws_bytes)
+    ref = oracle_attn_workload(wl)
+    e_warm = float(np.max(np.abs(out.cpu().numpy() - ref)))
+    e_full = float(np.max(np.abs(full().cpu().numpy() - ref)))
+    print(f"{name}: warm plan {warm.stats()} err {e_warm:.2e}; full plan {full.meta.stats()} err {e_full:.2e}",
+          flush=True)
+    assert e_warm <= TOL["bf16"] and e_full <= TOL["bf16"]
