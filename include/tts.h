@@ -381,8 +381,8 @@ tts_status tts_fork_tables(int32_t num_parents, const int32_t* parent_tables, in
  * parent_spec[p] speculative ones (the product sigma z[c] and the one with
  * parent_spec rounded to double before the sums). z: one standard-normal
  * draw per child (the caller's generator; entries of originals unused).
- * The paper leaves the spread open; this build's default reading is
- * sigma = 0.1. Writes child_lens[num_children] for tts_fork_tables.
+ * The paper leaves the spread open (sigma = 0.1 is the reading the tests
+ * use). Writes child_lens[num_children] for tts_fork_tables.
  * Errors (before anything is written): TTS_ERR_OUT_OF_RANGE for a bad parent,
  * TTS_ERR_INVALID_ARG for parent_spec outside [0, parent length], a
  * non-finite ratio or z, or sigma < 0. */

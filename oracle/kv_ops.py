@@ -21,12 +21,12 @@ full blocks and a private copy of the partially filled block it keeps
   that speculated keeps the fraction clip(R + sigma z, 0, 1) of the parent's
   speculative tokens, drawn from a normal distribution with mean R (the
   truncation ratio), rounded half up. The paper gives no spread and no
-  rounding: sigma (default reading 0.1) and the rounding are this build's
-  readings; the standard-normal draws z are inputs.
+  rounding: sigma (0.1 in the tests) and the rounding are readings of that
+  silence; the standard-normal draws z are inputs.
 
-The paper fixes none of the numeric policy: the fp8 scale rule is this
-build's reading (one fp32 scale per block and tensor, as the workload
-generator draws them).
+The paper fixes none of the numeric policy: the fp8 scale rule is a
+reading (one fp32 scale per block and tensor, as the workload generator
+draws them).
 """
 
 from __future__ import annotations
