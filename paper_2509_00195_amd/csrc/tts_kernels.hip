@@ -125,16 +125,16 @@ __device__ __forceinline__ float xlane_sum16(float x) {
 
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
-// Writes a row's partial state: m, l and o / (l s) in the partial layout
-// (fp16 elements with a power-of-two row scale s for bf16 and fp8 caches,
-// fp32 with s = 1 for fp32 caches; elements in lane order). Lane (ln, lq)
-// holds dimensions 16 t + 4 lq + j of row ln in o[t][j]; the four lanes of
-// a row call together (the scale is reduced across them), `active` says
-// whether the row exists.
+// A row's partial state: m, l and o / (l s) in the partial layout (fp16
+// elements with a power-of-two row scale s for bf16 and fp8 caches, fp32
+// with s = 1 for fp32 caches; elements in lane order). Lane (ln, lq) holds
+// dimensions 16 t + 4 lq + j of row ln in o[t][j]; the four lanes of a row
+// call together.
+//
+// partial_exp: the exponent e of s = 2^e for inv = 1 / l, reduced across
+// the row's lanes (every lane of the wave must call it).
 template <int D, int KV>
-__device__ __forceinline__ void write_partial(void* part_o, float* part_ml, int64_t prow, const f32x4 (&o)[D / 16],
-                                              float m, float l, int lq, bool active) {
-  const float inv = l > 0.f ? 1.f / l : 0.f;
+__device__ __forceinline__ int partial_exp(const f32x4 (&o)[D / 16], float inv) {
   int e = 0;
   if constexpr (KV != kKvF32) {
     float amax = 0.f;
@@ -148,7 +148,13 @@ __device__ __forceinline__ void write_partial(void* part_o, float* part_ml, int6
     // amax = f 2^e with f in [0.5, 1): every element over 2^e is in [-1, 1].
     if (amax > 0.f && amax <= 3.0e38f) e = __builtin_amdgcn_frexp_expf(amax);
   }
-  if (!active) return;
+  return e;
+}
+
+// store_partial: the row's stores, with inv and e from above.
+template <int D, int KV>
+__device__ __forceinline__ void store_partial(void* part_o, float* part_ml, int64_t prow, const f32x4 (&o)[D / 16],
+                                              float m, float l, float inv, int e, int lq) {
   if constexpr (KV != kKvF32) {
     uint32_t w[D / 8];
 #pragma unroll
@@ -172,6 +178,15 @@ __device__ __forceinline__ void write_partial(void* part_o, float* part_ml, int6
   const float m_out = (l > 0.f || m != m) ? m : kNegInf;
   if (lq == 0)
     *reinterpret_cast<f32x4*>(part_ml + prow * kPartMl) = f32x4{m_out, l, __builtin_ldexpf(1.f, e), 0.f};
+}
+
+// Both steps for one row; `active` says whether the row exists.
+template <int D, int KV>
+__device__ __forceinline__ void write_partial(void* part_o, float* part_ml, int64_t prow, const f32x4 (&o)[D / 16],
+                                              float m, float l, int lq, bool active) {
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  const int e = partial_exp<D, KV>(o, inv);
+  if (active) store_partial<D, KV>(part_o, part_ml, prow, o, m, l, inv, e, lq);
 }
 
 __device__ __forceinline__ int rl(int x, int i) { return __builtin_amdgcn_readlane(x, i); }
@@ -973,14 +988,24 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
           __syncthreads();
           if ((votes[0] | votes[1] | votes[2] | votes[3]) == 0) break;
         }
-        // Each wave writes the partial states of its own rows.
+        // Each wave writes the partial states of its own rows. The sums and
+        // scales of all its tiles first, in straight-line code, so that the
+        // tiles' cross-lane reductions overlap (a tile past the unit's rows
+        // holds l = 0 and zeros, and is not written).
+        float lw_[kWideTiles], inv_[kWideTiles];
+        int e_[kWideTiles];
+#pragma unroll
+        for (int i = 0; i < kWideTiles; ++i) lw_[i] = xlane_sum16(st[i].l);
+#pragma unroll
+        for (int i = 0; i < kWideTiles; ++i) inv_[i] = lw_[i] > 0.f ? 1.f / lw_[i] : 0.f;
+#pragma unroll
+        for (int i = 0; i < kWideTiles; ++i) e_[i] = partial_exp<D, KV>(st[i].o, inv_[i]);
 #pragma unroll
         for (int i = 0; i < kWideTiles; ++i) {
           if (wave + kWaves * i >= nt) continue;  // wave-uniform
           const int row = 16 * (wave + kWaves * i) + ln;
-          const float l = xlane_sum16(st[i].l);
           const int64_t prow = static_cast<int64_t>(kvh) * p.rows_per_head + prow0 + row;
-          write_partial<D, KV>(p.part_o, p.part_ml, prow, st[i].o, st[i].m, l, lq, row < nrows);
+          if (row < nrows) store_partial<D, KV>(p.part_o, p.part_ml, prow, st[i].o, st[i].m, lw_[i], inv_[i], e_[i], lq);
         }
         TTS_PROF_MARK(2, rec_idx);
         const int nu_rows_w = rfl(nu.nrows);
@@ -1178,6 +1203,11 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
 
     TTS_PROF_MARK(5, rec_idx);
     // ---- combine the four waves' states, tile r by wave r ------------------
+    // (Every tile's row sums first, in straight-line code, so that their
+    // cross-lane reductions overlap.)
+    float lt_[kTiles];
+#pragma unroll
+    for (int r = 0; r < kTiles; ++r) lt_[r] = xlane_sum16(st[r].l);
 #pragma unroll
     for (int r = 0; r < kTiles; ++r) {
       if (r < nt && r != wave) {
@@ -1185,10 +1215,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
 #pragma unroll
         for (int dt = 0; dt < D / 16; ++dt)
           *reinterpret_cast<f32x4*>(c + ln * G::comb_row + 16 * dt + 4 * lq) = st[r].o[dt];
-        const float lt = xlane_sum16(st[r].l);
         if (lq == 0) {
           c[kTok * G::comb_row + ln] = st[r].m;
-          c[kTok * G::comb_row + kTok + ln] = lt;
+          c[kTok * G::comb_row + kTok + ln] = lt_[r];
         }
       }
     }
@@ -1201,7 +1230,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
     for (int r = 0; r < kTiles; ++r) {
       if (r != wave || r >= nt) continue;
       const int row = 16 * r + ln;
-      const float own_l = xlane_sum16(st[r].l);
+      const float own_l = lt_[r];
       // A wave that saw no token of the row (l = 0: no pair of it, or every
       // score masked) keeps its initial reference; it must not set the
       // maximum, or a row whose scores all lie far below it would lose every
