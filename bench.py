@@ -37,8 +37,15 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
 def kernel_sha() -> str:
+    """Hash of the attention kernel's source and the device compile flags (a traffic record is valid only for the
+    code it was measured on)."""
+    from paper_2509_00195_amd.build import DEVICE
+
+    h = hashlib.sha256()
     with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+        h.update(f.read())
+    h.update(" ".join(DEVICE).encode())
+    return h.hexdigest()[:16]
 
 
 def parse():

@@ -3,7 +3,8 @@
     python -m paper_2509_00195_amd.build          # or __graft_entry__.build()
 
 Every HIP translation unit is compiled with packed-fp32 instruction
-selection disabled (``-target-feature -packed-fp32-ops``).
+selection disabled (``-target-feature -packed-fp32-ops``) and matrix
+instructions in their VGPR form (``-amdgpu-mfma-vgpr-form``).
 """
 
 from __future__ import annotations
@@ -23,7 +24,12 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}"]
 
-DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# -amdgpu-mfma-vgpr-form: matrix instructions accumulate in VGPRs. With
+# AGPR accumulators the attention kernel's pair loops copied every tile's
+# accumulators back into place at each branch join (hundreds of
+# v_accvgpr_mov per loop iteration); in VGPR form they accumulate in place.
+DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 SOURCES_HIP = ["tts_kernels.hip", "tts_kv.hip"]
 SOURCES_HOST = ["tts_meta.cpp", "tts_plan.cpp", "tts_alloc.cpp", "tts_sched.cpp", "tts_api.cpp"]
