@@ -33,17 +33,19 @@ sys.path.insert(0, ROOT)
 METRIC = "beam-tokens/s per decode step + % HBM peak (unique KV bytes), 1 MI355X"
 HBM_PEAK_GBS = 8000.0
 KERNEL_SRC = os.path.join(ROOT, "paper_2509_00195_amd", "csrc", "tts_kernels.hip")
+PLANNER_SRC = os.path.join(ROOT, "paper_2509_00195_amd", "csrc", "tts_plan.cpp")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
 def kernel_sha() -> str:
-    """Hash of the attention kernel's source and the device compile flags (a traffic record is valid only for the
-    code it was measured on)."""
+    """Hash of the attention kernel's source, the work planner's source and the device compile flags (a traffic
+    record is valid only for the code and the plans it was measured on)."""
     from paper_2509_00195_amd.build import DEVICE
 
     h = hashlib.sha256()
-    with open(KERNEL_SRC, "rb") as f:
-        h.update(f.read())
+    for src in (KERNEL_SRC, PLANNER_SRC):
+        with open(src, "rb") as f:
+            h.update(f.read())
     h.update(" ".join(DEVICE).encode())
     return h.hexdigest()[:16]
 

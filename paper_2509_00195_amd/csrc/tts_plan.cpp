@@ -43,13 +43,21 @@ namespace {
 // 0.113 us per block for each row tile a wave runs. (The narrow terms are
 // the least-squares fit scaled by 1.25: a plain fit under-predicts the
 // largest narrow units, which then finish last; the scale was chosen by
-// timing the kernel.) Other shapes scale the block terms by their bytes and
-// the tile term by the head size.
+// timing the kernel.) fp32 caches scale the block terms by their bytes and
+// every shape the tile term by the head size.
 constexpr double kUnitFixedUs = 4.9;
 constexpr double kNarrowUsPerByte = 0.2075 / 8192;
 constexpr double kRowUs = 0.08;  // per row of 256 + 272 bytes (query + partial state)
 constexpr double kWideUsPerByte = 0.193 / 8192;
 constexpr double kTileBlockUs = 0.113;  // per block and row tile of a wave, D = 128
+// fp8 caches: a block costs about what a bf16 block does (the products and
+// the conversion, not the bytes, set its time), so they take their own
+// terms, the least-squares fit to per-unit clock marks at the long-chain
+// batch (16 x 32 beams, fp8 KV, 1,772 units): narrow 3.30 us + 0.204 us
+// per block + 0.142 us per row, wide 4.60 us + 0.281 us per block + 0.093
+// us per block and row tile of a wave.
+constexpr double kFp8NarrowFixedUs = 3.30, kFp8NarrowBlockUs = 0.204, kFp8RowUs = 0.142;
+constexpr double kFp8WideFixedUs = 4.60, kFp8WideBlockUs = 0.281, kFp8TileBlockUs = 0.093;
 constexpr int kXcds = 8;  // workgroup k of a launch runs on XCD k % 8
 // The merge (a second launch): a fixed cost plus one round trip to memory
 // per kMergeBatch partial states of the beam with the most.
@@ -60,14 +68,19 @@ int tiles_of(int rows) { return (rows + 15) / 16; }
 
 struct CostModel {
   double blk_bytes, q_row_bytes, part_row_bytes, d_scale;
+  bool fp8 = false;
   double row_us() const { return kRowUs * (q_row_bytes + part_row_bytes) / 528.0; }
+  double narrow_fixed() const { return fp8 ? kFp8NarrowFixedUs : kUnitFixedUs; }
+  double wide_fixed() const { return fp8 ? kFp8WideFixedUs : kUnitFixedUs; }
   // Narrow units: the waves split the block pairs, every wave runs every tile.
   double narrow_us(int blocks, int rows) const {
+    if (fp8) return kFp8NarrowFixedUs + blocks * kFp8NarrowBlockUs + rows * kFp8RowUs;
     return kUnitFixedUs + blocks * blk_bytes * kNarrowUsPerByte + rows * row_us();
   }
   // Wide units: every wave runs every pair on its quarter of the tiles.
   double wide_us(int blocks, int rows) const {
     const int tpw = (tiles_of(rows) + 3) / 4;
+    if (fp8) return kFp8WideFixedUs + blocks * (kFp8WideBlockUs + tpw * kFp8TileBlockUs * d_scale);
     return kUnitFixedUs + blocks * (blk_bytes * kWideUsPerByte + tpw * kTileBlockUs * d_scale);
   }
   // Bytes a unit moves: its blocks, its query rows, its partial states.
@@ -133,6 +146,7 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, 
   // A partial state is written once and read once by the merge.
   cm.part_row_bytes = 2.0 * (shape.head_dim * (shape.kv_bytes == 4 ? 4.0 : 2.0) + 4 * kPartMl);
   cm.d_scale = shape.head_dim / 128.0;
+  cm.fp8 = shape.kv_bytes == 1;
 
   // ---- tree structure ----------------------------------------------------
   std::vector<std::vector<int32_t>> children(nseg), leaves(nseg);
@@ -412,9 +426,9 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, 
   // smallest predicted makespan over a grid of candidates is taken.
   double work = 0;
   for (const NItem& it : items)
-    if (!(it.flags & kEntExt)) work += cm.narrow_us(1, 0) - kUnitFixedUs;
+    if (!(it.flags & kEntExt)) work += cm.narrow_us(1, 0) - cm.narrow_fixed();
   for (int32_t s = 0; s < nseg; ++s)
-    if (wide[s]) work += cm.wide_us(m.seg_nblocks[s], RW * g) - kUnitFixedUs;
+    if (wide[s]) work += cm.wide_us(m.seg_nblocks[s], RW * g) - cm.wide_fixed();
   work = work * hkv / nbins;
   std::vector<Tmpl> tm;
   std::vector<std::vector<Work>> bins;
