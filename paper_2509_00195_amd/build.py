@@ -28,11 +28,8 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{os.path.join(ROOT, 'include')}", f"
 # AGPR accumulators the attention kernel's pair loops copied every tile's
 # accumulators back into place at each branch join (hundreds of
 # v_accvgpr_mov per loop iteration); in VGPR form they accumulate in place.
-DEVICE_NO_VGPR_FORM = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
-DEVICE = [*DEVICE_NO_VGPR_FORM, "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
-# The per-unit timestamp build (TTS_PROFILE_UNITS, tuning only) compiles
-# without the VGPR form: on that build the compiler's AGPR-copy rewrite pass
-# crashes.
+DEVICE = [f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 SOURCES_HIP = ["tts_kernels.hip", "tts_kv.hip"]
 SOURCES_HOST = ["tts_meta.cpp", "tts_plan.cpp", "tts_alloc.cpp", "tts_sched.cpp", "tts_api.cpp"]
@@ -54,8 +51,7 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
         objs = []
         for src in SOURCES_HIP:
             obj = os.path.join(tmp, src + ".o")
-            dev = DEVICE if "TTS_PROFILE_UNITS" not in defines else DEVICE_NO_VGPR_FORM
-            _run([HIPCC, *COMMON, *[f"-D{d}" for d in defines], *dev, "-c", os.path.join(CSRC, src), "-o", obj])
+            _run([HIPCC, *COMMON, *[f"-D{d}" for d in defines], *DEVICE, "-c", os.path.join(CSRC, src), "-o", obj])
             objs.append(obj)
         for src in SOURCES_HOST:
             obj = os.path.join(tmp, src + ".o")

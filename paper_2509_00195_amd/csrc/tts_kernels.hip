@@ -53,11 +53,13 @@ namespace tts {
 #ifdef TTS_PROFILE_UNITS
 // Per-unit timestamps for tuning builds only (indexed by record): start,
 // end of wave 0's block loop, end, the XCC / HW_ID registers, all waves
-// done, next unit issued, combine area written.
+// done, next unit issued, combine area written. (bf16 and fp8 kernels only:
+// with the marks in the fp32 kernels too, the compiler's AGPR-copy rewrite
+// pass crashes on the VGPR-form build.)
 constexpr int kProfSlots = 1 << 15;
 __device__ uint64_t g_prof[kProfSlots][8];
 #define TTS_PROF_MARK(k, i) \
-  do { if (threadIdx.x == 0 && (i) < kProfSlots) g_prof[(i)][k] = wall_clock64(); } while (0)
+  do { if (KV != kKvF32 && threadIdx.x == 0 && (i) < kProfSlots) g_prof[(i)][k] = wall_clock64(); } while (0)
 #else
 #define TTS_PROF_MARK(k, i) do {} while (0)
 #endif
@@ -1288,7 +1290,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
     }
 #ifdef TTS_PROFILE_UNITS
     TTS_PROF_MARK(2, rec_idx);
-    if (threadIdx.x == 0 && rec_idx < kProfSlots)
+    if (KV != kKvF32 && threadIdx.x == 0 && rec_idx < kProfSlots)
       g_prof[rec_idx][3] = (static_cast<uint64_t>(__builtin_amdgcn_s_getreg((3 << 11) | 20)) << 32) |
                            static_cast<uint32_t>(__builtin_amdgcn_s_getreg((31 << 11) | 4));
 #endif

@@ -58,6 +58,13 @@ constexpr double kTileBlockUs = 0.113;  // per block and row tile of a wave, D =
 // us per block and row tile of a wave.
 constexpr double kFp8NarrowFixedUs = 3.30, kFp8NarrowBlockUs = 0.204, kFp8RowUs = 0.142;
 constexpr double kFp8WideFixedUs = 4.60, kFp8WideBlockUs = 0.281, kFp8TileBlockUs = 0.093;
+// When the units outnumber the workgroups (chained plans, where nearly every
+// compute unit streams private blocks from HBM the whole time) a narrow
+// unit's blocks take longer than at the 7B 64-beam tree: at the straggler
+// batch the clock marks put narrow units at 1.24x the model and wide ones at
+// 1.07x. Chained plans scale the bf16 narrow block term by 1.3 (1.15 to 1.6
+// were timed; 1.3 was the fastest).
+constexpr double kChainedNarrowScale = 1.3;
 constexpr int kXcds = 8;  // workgroup k of a launch runs on XCD k % 8
 // The merge (a second launch): a fixed cost plus one round trip to memory
 // per kMergeBatch partial states of the beam with the most.
@@ -69,13 +76,14 @@ int tiles_of(int rows) { return (rows + 15) / 16; }
 struct CostModel {
   double blk_bytes, q_row_bytes, part_row_bytes, d_scale;
   bool fp8 = false;
+  double narrow_scale = 1.0;  // kChainedNarrowScale in chained plans
   double row_us() const { return kRowUs * (q_row_bytes + part_row_bytes) / 528.0; }
   double narrow_fixed() const { return fp8 ? kFp8NarrowFixedUs : kUnitFixedUs; }
   double wide_fixed() const { return fp8 ? kFp8WideFixedUs : kUnitFixedUs; }
   // Narrow units: the waves split the block pairs, every wave runs every tile.
   double narrow_us(int blocks, int rows) const {
     if (fp8) return kFp8NarrowFixedUs + blocks * kFp8NarrowBlockUs + rows * kFp8RowUs;
-    return kUnitFixedUs + blocks * blk_bytes * kNarrowUsPerByte + rows * row_us();
+    return kUnitFixedUs + narrow_scale * blocks * blk_bytes * kNarrowUsPerByte + rows * row_us();
   }
   // Wide units: every wave runs every pair on its quarter of the tiles.
   double wide_us(int blocks, int rows) const {
@@ -501,6 +509,7 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, 
       std::vector<Tmpl> cand;
       std::vector<std::vector<Work>> cbins;
       double best = -1;
+      cm.narrow_scale = kChainedNarrowScale;
       for (double f : {0.35, 0.5, 0.65, 0.8, 1.0, 1.2, 1.45, 1.75, 2.1, 2.5, 3.0, 4.0}) {
         int32_t cg = 0;
         make_templates(kUnitFixedUs + f * work, cand, cg);
