@@ -458,6 +458,11 @@ def main():
             "graph_call_us": graph_call_us,
             "q_len": qlen,
             "unique_kv_bytes": int(unique_kv),
+            # per call, beside the KV bytes: queries read, outputs written, the block-table rows the
+            # kernels read (the metadata's own buffer aside)
+            "q_bytes": int(wl.num_seqs * qlen * sh.num_q_heads * sh.head_dim * (4 if sh.q_dtype == "f32" else 2)),
+            "out_bytes": int(wl.num_seqs * qlen * sh.num_q_heads * sh.head_dim * 4),
+            "table_bytes": int(wl.block_tables.size * 4 + wl.num_seqs * 4),
             "logical_kv_bytes": int(logical_kv),
             "sharing": logical_kv / max(unique_kv, 1),
             "unique_kv_hbm_frac_per_call": unique_kv / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9),
