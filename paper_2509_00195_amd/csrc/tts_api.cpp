@@ -180,7 +180,7 @@ static tts_status build_meta_impl(int32_t num_reqs, const int32_t* req_seq_offse
     const auto& pl = m->plan;
     m->off_recs = 0;
     m->off_slot_tab = align256(m->off_recs + pl.recs.size() * sizeof(tts::UnitRec));
-    m->off_build = align256(m->off_slot_tab + pl.slot_tab.size() * 4);
+    m->off_build = align256(m->off_slot_tab + (pl.slot_tab.size() + tts::kSlotTabReadAhead) * 4);
     const size_t total = align256(m->off_build + S * 4);
     std::vector<unsigned char> img(total, 0);
     std::memcpy(img.data() + m->off_recs, pl.recs.data(), pl.recs.size() * sizeof(tts::UnitRec));

@@ -1353,6 +1353,10 @@ struct MergeRaw<4, false> {
 // that saw tokens (l_k > 0), w_k = l_k 2^(m_k - M), and e_k the stored
 // elements o_k / (l_k s_k):
 //   out = sum_k w_k s_k e_k / sum_k w_k.
+// A slot-table row of zeros for the paged path, which has no table (the
+// merges read their table entries without a branch).
+__device__ const int kZeroTabRow[kSlotTabReadAhead] = {};
+
 // Two kernels compute it; launch_merge picks by the number of rows.
 //
 // merge_row_kernel: D / 2 lanes per row (2 elements per lane), for batches
@@ -1375,22 +1379,19 @@ __global__ __launch_bounds__(kThreads) void merge_row_kernel(MergeParams p) {
   const int b = r / p.hq;
   const int h = r % p.hq;
   const int* tab = p.slot_tab ? p.slot_tab + static_cast<int64_t>(b) * p.slot_stride : nullptr;
-  int n;
+  // The row's inputs in one round trip: its table row (count and first
+  // kBatch entries; the paged path reads a row of zeros), its live length
+  // and its build-time length (the paged path, which has none, reads the
+  // live one again). No load waits for another.
+  const int* tabr = tab ? tab : kZeroTabRow;
   int ent[kBatch];
-  int64_t head_base;
-  if (tab) {
-    n = tab[0];
 #pragma unroll
-    for (int k = 0; k < kBatch; ++k) ent[k] = tab[1 + k];
-    head_base = static_cast<int64_t>(h / p.g) * p.rows_per_head + h % p.g;
-  } else {
-    n = p.paged_nsplit;
-#pragma unroll
-    for (int k = 0; k < kBatch; ++k) ent[k] = 0;
-    head_base = 0;
-  }
+  for (int k = 0; k < kBatch; ++k) ent[k] = tabr[1 + k];
+  const int n = tab ? tabr[0] : p.paged_nsplit;
+  const int64_t head_base = tab ? static_cast<int64_t>(h / p.g) * p.rows_per_head + h % p.g : 0;
   const int L = beam_len(p, b);
-  bool nan = p.build_len && L < p.build_len[b];
+  const int blen = (p.build_len ? p.build_len : p.seq_lens)[b];
+  bool nan = p.build_len && L < blen;
   float mx = kNegInf, den = 0.f;
   f32x2 acc = {0.f, 0.f};
   for (int k0 = 0; k0 < n; k0 += kBatch) {
@@ -1465,6 +1466,8 @@ constexpr int kMergeLanes = 16;
 // the GPU keeps resident at its occupancy); above, the sixteen-lane one.
 constexpr int kMergeRowKernelMaxRows = 4096;
 constexpr int kMergeTabChunks = 4;
+static_assert(1 + kMergeTabChunks * kMergeLanes <= kSlotTabReadAhead && 1 + kMergeBatch <= kSlotTabReadAhead,
+              "the merges' table read-ahead stays inside the table's padding");
 constexpr int kMergeThreads = 64;
 template <int D, bool F16>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p) {
@@ -1482,18 +1485,21 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(MergeParams p) {
   const int b = r / p.hq;
   const int h = r % p.hq;
   const int* tab = p.slot_tab ? p.slot_tab + static_cast<int64_t>(b) * p.slot_stride : nullptr;
-  const int n = tab ? tab[0] : p.paged_nsplit;
+  // The row's inputs in one round trip, as in merge_row_kernel: the count,
+  // the first kMergeTabChunks x 16 entries (read past the count, which the
+  // table's read-ahead zeros keep in bounds; entries past n are not used),
+  // the live and the build-time length.
+  const int* tabr = tab ? tab : kZeroTabRow;
+  int ent[kMergeTabChunks];
+#pragma unroll
+  for (int c = 0; c < kMergeTabChunks; ++c) ent[c] = tabr[1 + kBatch * c + j];
+  const int n = tab ? tabr[0] : p.paged_nsplit;
   const int head_base = tab ? (h / p.g) * p.rows_per_head + h % p.g : 0;
   // Partial row of slot k (k < n).
   auto slot_row = [&](int k, int entry) { return tab ? head_base + entry : (b * p.paged_nsplit + k) * p.hq + h; };
-  int ent[kMergeTabChunks];
-#pragma unroll
-  for (int c = 0; c < kMergeTabChunks; ++c) {
-    const int k = kBatch * c + j;
-    ent[c] = (tab && k < n) ? tab[1 + k] : 0;
-  }
   const int L = beam_len(p, b);
-  bool nan = p.build_len && L < p.build_len[b];
+  const int blen = (p.build_len ? p.build_len : p.seq_lens)[b];
+  bool nan = p.build_len && L < blen;
   float mx = kNegInf, den = 0.f;
   float acc[kEpl];
 #pragma unroll

@@ -115,6 +115,10 @@ struct AttnParams {
 // Slots the merge kernel reads per round trip (and the smallest slot-table
 // stride - 1, so that a beam's first round of slots is always in its row).
 constexpr int kMergeBatch = 16;
+// Readable int32 words after the start of any slot-table row (the table is
+// followed by this many zeros): the merges read a row's first entries in
+// the same round trip as its count, without waiting for the count.
+constexpr int kSlotTabReadAhead = 65;
 
 struct MergeParams {
   const void* part_o;
