@@ -1259,9 +1259,14 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
         } else {
           const float* c = comb_slot(w, r);
           l += lw[w] * f;
+          // All of the wave's reads first: read and add one at a time, the
+          // compiler waits for each read before issuing the next.
+          f32x4 t[D / 16];
 #pragma unroll
           for (int dt = 0; dt < D / 16; ++dt)
-            o[dt] += *reinterpret_cast<const f32x4*>(c + ln * G::comb_row + 16 * dt + 4 * lq) * f;
+            t[dt] = *reinterpret_cast<const f32x4*>(c + ln * G::comb_row + 16 * dt + 4 * lq);
+#pragma unroll
+          for (int dt = 0; dt < D / 16; ++dt) o[dt] += t[dt] * f;
         }
       }
       float m_fin = mx;
