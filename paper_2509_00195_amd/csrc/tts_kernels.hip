@@ -930,7 +930,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             load_quarter<D, KV>(qb, id0, id1, kbase, vbase, blk_stride, wave, ln, lq);
           }
           __syncthreads();  // every wave is done with the stage area (previous unit or attempt)
-          auto step = [&](Quarter<D, KV>& cur, Quarter<D, KV>& nxt, int pp) {
+          // tpw_c: the tiles per wave as a constant of this copy of the
+          // loop, or 0 for the count read at run time.
+          auto step = [&](auto tpw_c, Quarter<D, KV>& cur, Quarter<D, KV>& nxt, int pp) {
             unsigned char* stage = stages + (pp & 1) * SG::bytes;
             if constexpr (kRefill) {
               store_quarter<D, KV>(cur, stage, wave, lane);
@@ -956,9 +958,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
             pi.vs0 = cs.z;
             pi.vs1 = cs.w;
             if (pi.v1 == 0) mask_v<D, KV>(o, lq, pi.v0, pi.v1);
-            // The unit's tiles per wave (uniform): one straight-line block
-            // per count, so the compiler interleaves the tiles' products.
-            if (tpw >= kWideTiles) {
+            constexpr int kTpw = decltype(tpw_c)::value;
+            if constexpr (kTpw > 0) {
+#pragma unroll
+              for (int i = 0; i < kTpw; ++i) tile_step<D, KV, true>(o, qw[i], st[i], pi, wave + kWaves * i, ln, lq);
+            } else if (tpw >= kWideTiles) {
+              // The unit's tiles per wave (uniform): one straight-line block
+              // per count, so the compiler interleaves the tiles' products.
 #pragma unroll
               for (int i = 0; i < kWideTiles; ++i) tile_step<D, KV, true>(o, qw[i], st[i], pi, wave + kWaves * i, ln, lq);
             } else if (tpw == 2) {
@@ -968,10 +974,28 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
               tile_step<D, KV, true>(o, qw[0], st[0], pi, wave, ln, lq);
             }
           };
-          for (int pp = 0; pp < np; pp += 2) {
-            step(qa, qb, pp);
-            if (pp + 1 >= np) break;
-            step(qb, qa, pp + 1);
+          auto run = [&](auto tpw_c) {
+            for (int pp = 0; pp < np; pp += 2) {
+              step(tpw_c, qa, qb, pp);
+              if (pp + 1 >= np) break;
+              step(tpw_c, qb, qa, pp + 1);
+            }
+          };
+          // fp8: one copy of the loop per tiles-per-wave count. In the single
+          // loop the compiler copies the accumulators of the tiles that one
+          // branch updates and another does not at every join (~78 64-bit
+          // moves per pair at three tiles); the copies go away with the
+          // joins (long chain -2%). bf16 keeps the single loop: its per-count
+          // copies measured slower (7b64 +0.5 us, straggler +0.6 us).
+          if constexpr (KV == kKvFp8) {
+            if (tpw >= kWideTiles)
+              run(std::integral_constant<int, kWideTiles>{});
+            else if (tpw == 2)
+              run(std::integral_constant<int, 2>{});
+            else
+              run(std::integral_constant<int, 1>{});
+          } else {
+            run(std::integral_constant<int, 0>{});
           }
           if (attempt == 0) TTS_PROF_MARK(1, rec_idx);
           if (attempt > 0) break;
