@@ -76,6 +76,7 @@ struct WorkPlan {
   // whether the units were chained (more units than workgroups).
   double target_us = 0, work_us = 0;
   bool chained = false;
+  int32_t wide_rows = 0;  // the row cap of the wide units the plan chose
 };
 
 struct PlanShape {

@@ -8,8 +8,9 @@
 //
 // * Wide units. A segment shared by more beams than fit in a narrow unit
 //   (its rows exceed kMaxRows) is cut into row chunks of whole beams (up to
-//   kMaxWideRows rows: the four waves of the workgroup share every block
-//   through LDS, each taking a quarter of the row tiles) and, along its
+//   kMaxWideRows rows, or kAltWideRows where the cost model finds that plan
+//   cheaper: the four waves of the workgroup share every block through
+//   LDS, each taking a quarter of the row tiles) and, along its
 //   blocks, into pieces; every (piece, chunk) is a unit whose blocks apply
 //   to all of its rows. (fp32 caches use chunks of kMaxRows rows.) The
 //   chunks of one piece read the same blocks and are placed on one XCD.
@@ -66,6 +67,7 @@ constexpr double kFp8WideFixedUs = 4.60, kFp8WideBlockUs = 0.281, kFp8TileBlockU
 // were timed; 1.3 was the fastest).
 constexpr double kChainedNarrowScale = 1.3;
 constexpr int kXcds = 8;  // workgroup k of a launch runs on XCD k % 8
+constexpr int kAltWideRows = 128;  // the other wide-unit row cap the planner tries
 // The merge (a second launch): a fixed cost plus one round trip to memory
 // per kMergeBatch partial states of the beam with the most.
 constexpr double kMergeFixedUs = 3.2;
@@ -140,9 +142,13 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, 
   const int32_t hkv = shape.num_kv_heads;
   const int32_t bs = m.block_size;
   const int32_t RB = std::max(1, std::min(kMaxUnitBeams, kMaxRows / g));  // beams per narrow unit
-  // Beams per wide unit (bf16 and fp8 caches; fp32 caches use narrow-sized chunks).
+  // Beams per wide unit (bf16 and fp8 caches; fp32 caches use narrow-sized
+  // chunks): set per candidate row cap below.
   const bool wide_mode = shape.kv_bytes <= 2;
-  const int32_t RW = wide_mode ? std::max(1, std::min(kMaxWideBeams, kMaxWideRows / g)) : RB;
+  int32_t RW = RB;
+  auto wide_beams = [&](int32_t cap_rows) {
+    return wide_mode ? std::max(1, std::min(kMaxWideBeams, cap_rows / g)) : RB;
+  };
   const int32_t nseg = static_cast<int32_t>(m.seg_req.size());
   const int32_t nbins = std::max(1, shape.num_bins);
   P.num_bins = nbins;
@@ -432,12 +438,6 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, 
   // unit count only falls as T grows). When even the largest units
   // outnumber the workgroups, units are chained, and the target with the
   // smallest predicted makespan over a grid of candidates is taken.
-  double work = 0;
-  for (const NItem& it : items)
-    if (!(it.flags & kEntExt)) work += cm.narrow_us(1, 0) - cm.narrow_fixed();
-  for (int32_t s = 0; s < nseg; ++s)
-    if (wide[s]) work += cm.wide_us(m.seg_nblocks[s], RW * g) - cm.wide_fixed();
-  work = work * hkv / nbins;
   std::vector<Tmpl> tm;
   std::vector<std::vector<Work>> bins;
   int32_t ngroups = 0;
@@ -446,83 +446,138 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, 
     make_templates(T, tm, ngroups);
     return static_cast<int32_t>(tm.size());
   };
-  P.work_us = work;
-  if (warm && warm->target_us > 0 && warm->work_us > 0) {
-    // Warm re-plan: the earlier target, scaled with the work, raised while
-    // its units outnumber the workgroups (unless that plan was chained);
-    // one placement, no search.
-    double T = kUnitFixedUs + (warm->target_us - kUnitFixedUs) * (work / warm->work_us);
-    T = std::max(T, kUnitFixedUs + 1e-3);
-    if (!warm->chained)
-      for (int it = 0; it < 12 && units_at(T) > fit_units; ++it) T = kUnitFixedUs + 1.15 * (T - kUnitFixedUs);
-    units_at(T);
-    place(tm, ngroups, bins);
-    P.target_us = T;
-    P.chained = warm->chained;
-  } else {
-    // Upper bound of the search: a few times the average work per unit,
-    // raised while the units do not fit (one entry of many rows can cost
-    // more than that bound by its row term alone; without the raise such a
-    // batch would fall to the chained plans, with one tiny unit per entry).
-    double hi = kUnitFixedUs + 4.0 * work + 1.0;
-    for (int it = 0; it < 6 && units_at(hi) > fit_units; ++it) hi *= 2.0;
-    if (units_at(hi) <= fit_units) {
-      double lo = kUnitFixedUs;
-      for (int it = 0; it < 24; ++it) {
-        const double mid = 0.5 * (lo + hi);
-        if (units_at(mid) <= fit_units)
-          hi = mid;
-        else
-          lo = mid;
-      }
-      // Longer units mean fewer partial states per beam, so a cheaper merge:
-      // take the target (the smallest one's variable part scaled up) with the
-      // least modelled attention plus merge time.
-      std::vector<char> touched;
-      auto most_slots = [&](const std::vector<Tmpl>& t) {
-        std::vector<int32_t> cnt(S, 0);
-        for (const Tmpl& x : t) {
-          touched_beams(x, g, &touched);
-          for (int32_t i = 0; i < x.hi - x.lo; ++i)
-            if (touched[i]) ++cnt[m.perm[x.lo + i]];
-        }
-        return S > 0 ? *std::max_element(cnt.begin(), cnt.end()) : 0;
-      };
-      const double t_min = hi;
-      double best_T = t_min, best_est = -1;
-      for (double f : {1.0, 1.5, 2.0, 3.0, 4.0, 6.0}) {
-        const double T = kUnitFixedUs + f * (t_min - kUnitFixedUs);
-        if (units_at(T) > fit_units) continue;
-        double ms = 0;
-        for (const Tmpl& x : tm) ms = std::max(ms, x.cost);
-        const int32_t slots = most_slots(tm);
-        const double est = ms + kMergeFixedUs + kMergeBatchUs * ((slots + kMergeBatch - 1) / kMergeBatch);
-        if (best_est < 0 || est < best_est) {
-          best_est = est;
-          best_T = T;
-        }
-      }
-      units_at(best_T);
-      place(tm, ngroups, bins);
-      P.target_us = best_T;
+  // One search at the current RW: fills tm, bins, ngroups and the plan's
+  // target, work and chaining; returns the modelled time it minimised (the
+  // longest unit plus the merge for plans that fit the workgroups, the
+  // largest workgroup load for chained ones).
+  auto search = [&]() {
+    cm.narrow_scale = 1.0;
+    double est = 0;
+    double work = 0;
+    for (const NItem& it : items)
+      if (!(it.flags & kEntExt)) work += cm.narrow_us(1, 0) - cm.narrow_fixed();
+    for (int32_t s = 0; s < nseg; ++s)
+      if (wide[s]) work += cm.wide_us(m.seg_nblocks[s], RW * g) - cm.wide_fixed();
+    work = work * hkv / nbins;
+    P.work_us = work;
+    P.chained = false;
+    if (warm && warm->target_us > 0 && warm->work_us > 0) {
+      // Warm re-plan: the earlier target, scaled with the work, raised while
+      // its units outnumber the workgroups (unless that plan was chained);
+      // one placement, no search.
+      double T = kUnitFixedUs + (warm->target_us - kUnitFixedUs) * (work / warm->work_us);
+      T = std::max(T, kUnitFixedUs + 1e-3);
+      if (!warm->chained)
+        for (int it = 0; it < 12 && units_at(T) > fit_units; ++it) T = kUnitFixedUs + 1.15 * (T - kUnitFixedUs);
+      units_at(T);
+      est = place(tm, ngroups, bins);
+      P.target_us = T;
+      P.chained = warm->chained;
     } else {
-      std::vector<Tmpl> cand;
-      std::vector<std::vector<Work>> cbins;
-      double best = -1;
-      cm.narrow_scale = kChainedNarrowScale;
-      for (double f : {0.35, 0.5, 0.65, 0.8, 1.0, 1.2, 1.45, 1.75, 2.1, 2.5, 3.0, 4.0}) {
-        int32_t cg = 0;
-        make_templates(kUnitFixedUs + f * work, cand, cg);
-        const double ms = place(cand, cg, cbins);
-        if (best < 0 || ms < best) {
-          best = ms;
-          tm.swap(cand);
-          bins.swap(cbins);
-          ngroups = cg;
-          P.target_us = kUnitFixedUs + f * work;
+      // Upper bound of the search: a few times the average work per unit,
+      // raised while the units do not fit (one entry of many rows can cost
+      // more than that bound by its row term alone; without the raise such a
+      // batch would fall to the chained plans, with one tiny unit per entry).
+      double hi = kUnitFixedUs + 4.0 * work + 1.0;
+      for (int it = 0; it < 6 && units_at(hi) > fit_units; ++it) hi *= 2.0;
+      if (units_at(hi) <= fit_units) {
+        double lo = kUnitFixedUs;
+        for (int it = 0; it < 24; ++it) {
+          const double mid = 0.5 * (lo + hi);
+          if (units_at(mid) <= fit_units)
+            hi = mid;
+          else
+            lo = mid;
         }
+        // Longer units mean fewer partial states per beam, so a cheaper merge:
+        // take the target (the smallest one's variable part scaled up) with the
+        // least modelled attention plus merge time.
+        std::vector<char> touched;
+        auto most_slots = [&](const std::vector<Tmpl>& t) {
+          std::vector<int32_t> cnt(S, 0);
+          for (const Tmpl& x : t) {
+            touched_beams(x, g, &touched);
+            for (int32_t i = 0; i < x.hi - x.lo; ++i)
+              if (touched[i]) ++cnt[m.perm[x.lo + i]];
+          }
+          return S > 0 ? *std::max_element(cnt.begin(), cnt.end()) : 0;
+        };
+        const double t_min = hi;
+        double best_T = t_min, best_est = -1;
+        for (double f : {1.0, 1.5, 2.0, 3.0, 4.0, 6.0}) {
+          const double T = kUnitFixedUs + f * (t_min - kUnitFixedUs);
+          if (units_at(T) > fit_units) continue;
+          double ms = 0;
+          for (const Tmpl& x : tm) ms = std::max(ms, x.cost);
+          const int32_t slots = most_slots(tm);
+          const double est = ms + kMergeFixedUs + kMergeBatchUs * ((slots + kMergeBatch - 1) / kMergeBatch);
+          if (best_est < 0 || est < best_est) {
+            best_est = est;
+            best_T = T;
+          }
+        }
+        units_at(best_T);
+        place(tm, ngroups, bins);
+        P.target_us = best_T;
+        est = best_est;
+      } else {
+        std::vector<Tmpl> cand;
+        std::vector<std::vector<Work>> cbins;
+        double best = -1;
+        cm.narrow_scale = kChainedNarrowScale;
+        for (double f : {0.35, 0.5, 0.65, 0.8, 1.0, 1.2, 1.45, 1.75, 2.1, 2.5, 3.0, 4.0}) {
+          int32_t cg = 0;
+          make_templates(kUnitFixedUs + f * work, cand, cg);
+          const double ms = place(cand, cg, cbins);
+          if (best < 0 || ms < best) {
+            best = ms;
+            tm.swap(cand);
+            bins.swap(cbins);
+            ngroups = cg;
+            P.target_us = kUnitFixedUs + f * work;
+          }
+        }
+        P.chained = true;
+        est = best;
       }
-      P.chained = true;
+    }
+    return est;
+  };
+
+  // Wide units of up to kMaxWideRows rows (three row tiles per wave), or of
+  // up to kAltWideRows (two): fewer rows per chunk means more chunks that
+  // stage the same blocks, but shorter units to balance. The model picks
+  // (7B 64-beam tree: 192 rows; balanced tree and straggler batch: 128,
+  // each 1.4 us per call faster than with 192), comparing plans of one kind
+  // only (both fit the workgroups, or both are chained). A warm re-plan
+  // keeps the earlier plan's cap.
+  if (warm && warm->target_us > 0 && warm->work_us > 0) {
+    P.wide_rows = warm->wide_rows > 0 ? warm->wide_rows : kMaxWideRows;
+    RW = wide_beams(P.wide_rows);
+    search();
+  } else {
+    P.wide_rows = kMaxWideRows;
+    RW = wide_beams(kMaxWideRows);
+    double best = search();
+    if (wide_mode && wide_beams(kAltWideRows) != RW) {
+      std::vector<Tmpl> tm0 = tm;
+      std::vector<std::vector<Work>> bins0 = bins;
+      const int32_t ngroups0 = ngroups;
+      const double target0 = P.target_us, work0 = P.work_us;
+      const bool chained0 = P.chained;
+      RW = wide_beams(kAltWideRows);
+      const double alt = search();
+      if (P.chained == chained0 && alt < best) {
+        P.wide_rows = kAltWideRows;
+      } else {
+        RW = wide_beams(kMaxWideRows);
+        tm.swap(tm0);
+        bins.swap(bins0);
+        ngroups = ngroups0;
+        P.target_us = target0;
+        P.work_us = work0;
+        P.chained = chained0;
+      }
     }
   }
 

@@ -107,3 +107,25 @@ def test_plan_argument_errors():
     bad = np.where(wl.block_tables == wl.block_tables[0, 0], wl.num_blocks + 5, wl.block_tables).astype(np.int32)
     with pytest.raises(tts.TTSError):
         tts.tts_plan_units_host(wl.req_seq_offsets, bad, wl.seq_lens, BS, wl.num_blocks, desc, 8)
+
+
+def wide_unit_rows(name, nbins=256):
+    """Query rows of each wide unit in the seed-0 plan of a config."""
+    cfg = CONFIGS[name]
+    rows, _ = plan_rows(tables_of(cfg, 0), cfg.shape, nbins)
+    unit, beam, flags = rows[:, 0], rows[:, 3], rows[:, 6]
+    wide = (flags & PLAN_WIDE) != 0
+    g = cfg.shape.num_q_heads // cfg.shape.num_kv_heads
+    beams = {}
+    for u, b in zip(unit[wide], beam[wide]):
+        beams.setdefault(int(u), set()).add(int(b))
+    return [g * len(v) for v in beams.values()]
+
+
+def test_wide_row_cap_is_chosen_per_batch():
+    """The planner models a batch with wide units of up to 192 rows (three row tiles per wave) and of up to 128
+    (two) and keeps the cheaper plan: 192 for the 7B 64-beam tree, 128 for the balanced tree."""
+    r = wide_unit_rows("7b64")
+    assert r and 128 < max(r) <= 192
+    r = wide_unit_rows("7b64_balanced")
+    assert r and max(r) <= 128
