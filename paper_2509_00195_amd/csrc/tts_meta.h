@@ -76,7 +76,8 @@ struct WorkPlan {
   // whether the units were chained (more units than workgroups).
   double target_us = 0, work_us = 0;
   bool chained = false;
-  int32_t wide_rows = 0;  // the row cap of the wide units the plan chose
+  int32_t wide_rows = 0;    // the row caps of the wide and the narrow units
+  int32_t narrow_rows = 0;  // the plan chose
 };
 
 struct PlanShape {

@@ -19,9 +19,10 @@
 //   blocks, then its subtrees and the tails of the beams ending at it, in
 //   canonical order). Consecutive entries of that list always cover a
 //   contiguous range of beams, so the list is cut into units of at most
-//   kMaxUnitBeams beams / kMaxRows rows / kMaxEntries entries and about
-//   equal cost: a small subtree with its tails becomes one unit and one
-//   partial state per beam instead of one per segment.
+//   kMaxUnitBeams beams / kMaxRows rows (kAltRows where the cost model
+//   finds that plan cheaper) / kMaxEntries entries and about equal cost: a
+//   small subtree with its tails becomes one unit and one partial state per
+//   beam instead of one per segment.
 //
 // Units are replicated per KV head, grouped, spread over the XCDs longest
 // first and then over each XCD's workgroups longest first.
@@ -68,6 +69,7 @@ constexpr double kFp8WideFixedUs = 4.60, kFp8WideBlockUs = 0.281, kFp8TileBlockU
 constexpr double kChainedNarrowScale = 1.3;
 constexpr int kXcds = 8;  // workgroup k of a launch runs on XCD k % 8
 constexpr int kAltWideRows = 128;  // the other wide-unit row cap the planner tries
+constexpr int kAltRows = 42;       // the other narrow-unit row cap (plans that fit the workgroups)
 // The merge (a second launch): a fixed cost plus one round trip to memory
 // per kMergeBatch partial states of the beam with the most.
 constexpr double kMergeFixedUs = 3.2;
@@ -141,7 +143,9 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, 
   const int32_t g = shape.num_q_heads / shape.num_kv_heads;
   const int32_t hkv = shape.num_kv_heads;
   const int32_t bs = m.block_size;
-  const int32_t RB = std::max(1, std::min(kMaxUnitBeams, kMaxRows / g));  // beams per narrow unit
+  // Beams per narrow unit: set per candidate row cap below.
+  auto narrow_beams = [&](int32_t cap_rows) { return std::max(1, std::min(kMaxUnitBeams, cap_rows / g)); };
+  int32_t RB = narrow_beams(kMaxRows);
   // Beams per wide unit (bf16 and fp8 caches; fp32 caches use narrow-sized
   // chunks): set per candidate row cap below.
   const bool wide_mode = shape.kv_bytes <= 2;
@@ -183,7 +187,6 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, 
       top[req_of_pos(pos)].push_back({pos, -1 - pos});
   }
   std::vector<char> wide(nseg, 0);
-  for (int32_t s = 0; s < nseg; ++s) wide[s] = (m.seg_beam_end[s] - m.seg_beam_begin[s]) > RB;
   auto seg_block = [&](int32_t s, int32_t j) {
     const int32_t b = m.perm[m.seg_beam_begin[s]];
     return m.tables[static_cast<size_t>(b) * m.max_blocks + m.seg_lblock_begin[s] + j];
@@ -202,33 +205,39 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, 
     }
     items.push_back({0, pos, pos + 1, 1, kEntExt});
   };
-  // Iterative walk: a stack of (segment, or -1 - leaf position).
+  // Iterative walk: a stack of (segment, or -1 - leaf position). Which
+  // segments are wide (more beams than a narrow unit takes) depends on RB,
+  // so the list is made again for each narrow row cap.
   std::vector<int32_t> stack;
   auto push_sorted = [&](std::vector<std::pair<int32_t, int32_t>>& v) {
     std::sort(v.begin(), v.end());
     for (auto it = v.rbegin(); it != v.rend(); ++it) stack.push_back(it->second);
   };
   std::vector<std::pair<int32_t, int32_t>> tmp;
-  for (auto& t : top) {
-    push_sorted(t);
-    while (!stack.empty()) {
-      const int32_t x = stack.back();
-      stack.pop_back();
-      if (x < 0) {
-        emit_tail(-1 - x);
-        continue;
+  auto list_items = [&]() {
+    for (int32_t s = 0; s < nseg; ++s) wide[s] = (m.seg_beam_end[s] - m.seg_beam_begin[s]) > RB;
+    items.clear();
+    for (auto& t : top) {
+      push_sorted(t);
+      while (!stack.empty()) {
+        const int32_t x = stack.back();
+        stack.pop_back();
+        if (x < 0) {
+          emit_tail(-1 - x);
+          continue;
+        }
+        const int32_t bb = m.seg_beam_begin[x], be = m.seg_beam_end[x];
+        if (!wide[x]) {
+          for (int32_t j = 0; j < m.seg_nblocks[x]; ++j)
+            items.push_back({seg_block(x, j), bb, be, bs, 0u});
+        }
+        tmp.clear();
+        for (int32_t c : children[x]) tmp.push_back({m.seg_beam_begin[c], c});
+        for (int32_t pos : leaves[x]) tmp.push_back({pos, -1 - pos});
+        push_sorted(tmp);
       }
-      const int32_t bb = m.seg_beam_begin[x], be = m.seg_beam_end[x];
-      if (!wide[x]) {
-        for (int32_t j = 0; j < m.seg_nblocks[x]; ++j)
-          items.push_back({seg_block(x, j), bb, be, bs, 0u});
-      }
-      tmp.clear();
-      for (int32_t c : children[x]) tmp.push_back({m.seg_beam_begin[c], c});
-      for (int32_t pos : leaves[x]) tmp.push_back({pos, -1 - pos});
-      push_sorted(tmp);
     }
-  }
+  };
 
   // ---- units for a target unit time T ------------------------------------
   // A wide segment of G beams and n blocks is cut into C row chunks and P
@@ -544,41 +553,60 @@ void build_work_plan(const HostMeta& m, const PlanShape& shape, WorkPlan* plan, 
     return est;
   };
 
-  // Wide units of up to kMaxWideRows rows (three row tiles per wave), or of
-  // up to kAltWideRows (two): fewer rows per chunk means more chunks that
-  // stage the same blocks, but shorter units to balance. The model picks
-  // (7B 64-beam tree: 192 rows; balanced tree and straggler batch: 128,
-  // each 1.4 us per call faster than with 192), comparing plans of one kind
-  // only (both fit the workgroups, or both are chained). A warm re-plan
-  // keeps the earlier plan's cap.
+  // Row caps. Wide units of up to kMaxWideRows rows (three row tiles per
+  // wave) or of up to kAltWideRows (two): fewer rows per chunk means more
+  // chunks that stage the same blocks, but shorter units to balance. Then,
+  // for plans that fit the workgroups, narrow units of up to kAltRows rows
+  // instead of kMaxRows: more, shorter units. The model picks, comparing
+  // plans of one kind only (both fit the workgroups, or both are chained);
+  // a candidate must model strictly faster. Measured: 7B 64-beam tree 192 /
+  // 64 rows; balanced tree and straggler batch 128-row wide units (-1.3 and
+  // -1.7 us per call); 1.5B 16-beam tree 42-row narrow units (-1.5 us). A
+  // warm re-plan keeps the earlier plan's caps.
   if (warm && warm->target_us > 0 && warm->work_us > 0) {
     P.wide_rows = warm->wide_rows > 0 ? warm->wide_rows : kMaxWideRows;
+    P.narrow_rows = warm->narrow_rows > 0 ? warm->narrow_rows : kMaxRows;
+    RB = narrow_beams(P.narrow_rows);
     RW = wide_beams(P.wide_rows);
+    list_items();
     search();
   } else {
     P.wide_rows = kMaxWideRows;
+    P.narrow_rows = kMaxRows;
     RW = wide_beams(kMaxWideRows);
+    list_items();
     double best = search();
-    if (wide_mode && wide_beams(kAltWideRows) != RW) {
+    // Runs the search at caps (wide, narrow) and keeps it if it models
+    // faster than the plan at hand, else restores that plan.
+    auto try_caps = [&](int32_t wide_rows, int32_t narrow_rows) {
       std::vector<Tmpl> tm0 = tm;
       std::vector<std::vector<Work>> bins0 = bins;
-      const int32_t ngroups0 = ngroups;
+      const int32_t ngroups0 = ngroups, RW0 = RW, RB0 = RB;
       const double target0 = P.target_us, work0 = P.work_us;
       const bool chained0 = P.chained;
-      RW = wide_beams(kAltWideRows);
+      RB = narrow_beams(narrow_rows);
+      RW = wide_beams(wide_rows);
+      if (RB != RB0) list_items();
       const double alt = search();
       if (P.chained == chained0 && alt < best) {
-        P.wide_rows = kAltWideRows;
-      } else {
-        RW = wide_beams(kMaxWideRows);
-        tm.swap(tm0);
-        bins.swap(bins0);
-        ngroups = ngroups0;
-        P.target_us = target0;
-        P.work_us = work0;
-        P.chained = chained0;
+        best = alt;
+        P.wide_rows = wide_rows;
+        P.narrow_rows = narrow_rows;
+        return;
       }
-    }
+      RW = RW0;
+      const bool relist = RB != RB0;
+      RB = RB0;
+      if (relist) list_items();
+      tm.swap(tm0);
+      bins.swap(bins0);
+      ngroups = ngroups0;
+      P.target_us = target0;
+      P.work_us = work0;
+      P.chained = chained0;
+    };
+    if (wide_mode && wide_beams(kAltWideRows) != RW) try_caps(kAltWideRows, P.narrow_rows);
+    if (!P.chained && narrow_beams(kAltRows) != RB) try_caps(P.wide_rows, kAltRows);
   }
 
   // ---- partial rows and merge lists ----------------------------------------

@@ -109,23 +109,27 @@ def test_plan_argument_errors():
         tts.tts_plan_units_host(wl.req_seq_offsets, bad, wl.seq_lens, BS, wl.num_blocks, desc, 8)
 
 
-def wide_unit_rows(name, nbins=256):
-    """Query rows of each wide unit in the seed-0 plan of a config."""
+def unit_rows(name, wide, nbins=256):
+    """Query rows of each wide (or each narrow) unit in the seed-0 plan of a config."""
     cfg = CONFIGS[name]
     rows, _ = plan_rows(tables_of(cfg, 0), cfg.shape, nbins)
     unit, beam, flags = rows[:, 0], rows[:, 3], rows[:, 6]
-    wide = (flags & PLAN_WIDE) != 0
+    sel = ((flags & PLAN_WIDE) != 0) == wide
     g = cfg.shape.num_q_heads // cfg.shape.num_kv_heads
     beams = {}
-    for u, b in zip(unit[wide], beam[wide]):
+    for u, b in zip(unit[sel], beam[sel]):
         beams.setdefault(int(u), set()).add(int(b))
     return [g * len(v) for v in beams.values()]
 
 
-def test_wide_row_cap_is_chosen_per_batch():
+def test_row_caps_are_chosen_per_batch():
     """The planner models a batch with wide units of up to 192 rows (three row tiles per wave) and of up to 128
-    (two) and keeps the cheaper plan: 192 for the 7B 64-beam tree, 128 for the balanced tree."""
-    r = wide_unit_rows("7b64")
+    (two), and a batch that fits the workgroups with narrow units of up to 64 rows and of up to 42, and keeps
+    the cheaper plan: 192 / 64 for the 7B 64-beam tree, 128-row wide units for the balanced tree, 42-row
+    narrow units for the 1.5B 16-beam tree."""
+    r = unit_rows("7b64", wide=True)
     assert r and 128 < max(r) <= 192
-    r = wide_unit_rows("7b64_balanced")
+    assert 42 < max(unit_rows("7b64", wide=False)) <= 64
+    r = unit_rows("7b64_balanced", wide=True)
     assert r and max(r) <= 128
+    assert max(unit_rows("1p5b16", wide=False)) <= 42
