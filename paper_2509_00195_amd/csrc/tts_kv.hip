@@ -84,10 +84,10 @@ struct AppendParams {
 // fit it and the block's earlier codes are re-encoded under the new scale.
 template <typename At>
 __device__ void append_fp8(const uint16_t* src, int n, int slot, float* scale_p, At at, int D, float* red) {
+  const float s_old = *scale_p;  // read ahead of the reduction's barriers, with the token
   float a = 0.f;
   for (int i = threadIdx.x; i < n; i += kKvThreads) a = fmaxf(a, __builtin_fabsf(bf16_to_f32(src[i])));
   a = block_max(a, red);
-  const float s_old = *scale_p;
   float s = s_old;
   bool requant = false;
   if (slot == 0) {
@@ -99,11 +99,14 @@ __device__ void append_fp8(const uint16_t* src, int n, int slot, float* scale_p,
   if (requant) {
     for (int i = threadIdx.x; i < n; i += kKvThreads) {
       const int h = i / D, d = i % D;
-      for (int j = 0; j < slot; ++j) {
-        uint8_t* c = at(h, j, d);
-        const float v = e4m3_decode(*c) * s_old;
-        *c = static_cast<uint8_t>(e4m3_encode(v / s));
-      }
+      // All of the element's earlier codes are read first, so that their
+      // loads are in flight together, then re-encoded and written.
+      uint32_t old[kSlots];
+#pragma unroll
+      for (int j = 0; j < kSlots; ++j) old[j] = j < slot ? *at(h, j, d) : 0u;
+#pragma unroll
+      for (int j = 0; j < kSlots; ++j)
+        if (j < slot) *at(h, j, d) = static_cast<uint8_t>(e4m3_encode(e4m3_decode(old[j]) * s_old / s));
     }
   }
   for (int i = threadIdx.x; i < n; i += kKvThreads) {
@@ -114,13 +117,15 @@ __device__ void append_fp8(const uint16_t* src, int n, int slot, float* scale_p,
   if (threadIdx.x == 0) *scale_p = s;
 }
 
-// One workgroup per beam: the beam's current token (position seq_len - 1)
-// into slot (seq_len - 1) % 16 of its block. Beams with seq_len 0, a block
-// index past the table row or a block id outside the pool write nothing.
+// Two workgroups per beam, one for K and one for V (their dependent steps
+// run side by side): the beam's current token (position seq_len - 1) into
+// slot (seq_len - 1) % 16 of its block. Beams with seq_len 0, a block index
+// past the table row or a block id outside the pool write nothing.
 template <int KV>  // 0 fp32, 1 bf16, 2 fp8
 __global__ __launch_bounds__(kKvThreads) void append_kernel(AppendParams p) {
   __shared__ float red[kKvThreads / 64];
-  const int b = blockIdx.x;
+  const int b = static_cast<int>(blockIdx.x >> 1);
+  const bool is_v = (blockIdx.x & 1) != 0;
   const int L = p.seq_lens[b];
   if (L <= 0) return;
   const int t = L - 1;
@@ -134,24 +139,21 @@ __global__ __launch_bounds__(kKvThreads) void append_kernel(AppendParams p) {
   auto k_at = [&](int h, int j, int d) { return ((base + h) * kSlots + j) * D + d; };
   auto v_at = [&](int h, int j, int d) { return ((base + h) * D + d) * kSlots + j; };
   if constexpr (KV == 0) {
-    const float* kn = static_cast<const float*>(p.k_new) + src0;
-    const float* vn = static_cast<const float*>(p.v_new) + src0;
-    for (int i = threadIdx.x; i < n; i += kKvThreads) {
-      static_cast<float*>(p.k_cache)[k_at(i / D, slot, i % D)] = kn[i];
-      static_cast<float*>(p.v_cache)[v_at(i / D, slot, i % D)] = vn[i];
-    }
+    const float* src = static_cast<const float*>(is_v ? p.v_new : p.k_new) + src0;
+    float* dst = static_cast<float*>(is_v ? p.v_cache : p.k_cache);
+    for (int i = threadIdx.x; i < n; i += kKvThreads)
+      dst[is_v ? v_at(i / D, slot, i % D) : k_at(i / D, slot, i % D)] = src[i];
   } else if constexpr (KV == 1) {
-    const uint16_t* kn = static_cast<const uint16_t*>(p.k_new) + src0;
-    const uint16_t* vn = static_cast<const uint16_t*>(p.v_new) + src0;
-    for (int i = threadIdx.x; i < n; i += kKvThreads) {
-      static_cast<uint16_t*>(p.k_cache)[k_at(i / D, slot, i % D)] = kn[i];
-      static_cast<uint16_t*>(p.v_cache)[v_at(i / D, slot, i % D)] = vn[i];
-    }
-  } else {
+    const uint16_t* src = static_cast<const uint16_t*>(is_v ? p.v_new : p.k_new) + src0;
+    uint16_t* dst = static_cast<uint16_t*>(is_v ? p.v_cache : p.k_cache);
+    for (int i = threadIdx.x; i < n; i += kKvThreads)
+      dst[is_v ? v_at(i / D, slot, i % D) : k_at(i / D, slot, i % D)] = src[i];
+  } else if (!is_v) {
     uint8_t* kc = static_cast<uint8_t*>(p.k_cache);
-    uint8_t* vc = static_cast<uint8_t*>(p.v_cache);
     append_fp8(static_cast<const uint16_t*>(p.k_new) + src0, n, slot, p.k_scale + blk,
                [&](int h, int j, int d) { return kc + k_at(h, j, d); }, D, red);
+  } else {
+    uint8_t* vc = static_cast<uint8_t*>(p.v_cache);
     append_fp8(static_cast<const uint16_t*>(p.v_new) + src0, n, slot, p.v_scale + blk,
                [&](int h, int j, int d) { return vc + v_at(h, j, d); }, D, red);
   }
@@ -195,11 +197,11 @@ hipError_t launch_append(const void* k_new, const void* v_new, const int32_t* bl
   AppendParams p{k_new, v_new, block_tables, seq_lens, k_cache, v_cache, k_scale, v_scale,
                  max_blocks, num_blocks, hkv, head_dim};
   if (kv_kind == 0)
-    hipLaunchKernelGGL(append_kernel<0>, dim3(num_seqs), dim3(kKvThreads), 0, stream, p);
+    hipLaunchKernelGGL(append_kernel<0>, dim3(2 * num_seqs), dim3(kKvThreads), 0, stream, p);
   else if (kv_kind == 1)
-    hipLaunchKernelGGL(append_kernel<1>, dim3(num_seqs), dim3(kKvThreads), 0, stream, p);
+    hipLaunchKernelGGL(append_kernel<1>, dim3(2 * num_seqs), dim3(kKvThreads), 0, stream, p);
   else
-    hipLaunchKernelGGL(append_kernel<2>, dim3(num_seqs), dim3(kKvThreads), 0, stream, p);
+    hipLaunchKernelGGL(append_kernel<2>, dim3(2 * num_seqs), dim3(kKvThreads), 0, stream, p);
   return hipGetLastError();
 }
 
