@@ -296,9 +296,9 @@ tts_status tts_prefix_verify_attn(const tts_attn_desc* d, const tts_prefix_meta*
  * them separately (to overlap the merge with other work, or to time the
  * attention kernel alone). tts_prefix_decode_partials runs the work units
  * and leaves one partial softmax state (reference max, sum, and the output
- * row normalised by that sum, in fp16 with a power-of-two row scale for
- * bf16 and fp8 caches, in fp32 for fp32 caches) per (beam, query head,
- * slot) in the workspace;
+ * row: for bf16 and fp8 caches in fp16, divided by a power of two, with a
+ * factor that takes it to the row normalised by the sum; for fp32 caches
+ * normalised, in fp32) per (beam, query head, slot) in the workspace;
  * tts_prefix_decode_merge combines each beam's states, in slot order, into
  * out. Arguments and rules are those of tts_prefix_decode_attn; the merge
  * must follow the partials call on the same workspace in stream order, with

@@ -127,16 +127,17 @@ __device__ __forceinline__ float xlane_sum16(float x) {
 
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
-// A row's partial state: m, l and o / (l s) in the partial layout (fp16
-// elements with a power-of-two row scale s for bf16 and fp8 caches, fp32
-// with s = 1 for fp32 caches; elements in lane order). Lane (ln, lq) holds
-// dimensions 16 t + 4 lq + j of row ln in o[t][j]; the four lanes of a row
-// call together.
+// A row's partial state: m, l, the output row and its factor z, with
+// (stored element) x z = o / l. For bf16 and fp8 caches the elements are o
+// scaled by a power of two, 2^-e, in fp16 (z = 2^e / l); for fp32 caches
+// they are o / l in fp32 (z = 1). Elements in lane order: lane (ln, lq)
+// holds dimensions 16 t + 4 lq + j of row ln in o[t][j]; the four lanes of
+// a row call together.
 //
-// partial_exp: the exponent e of s = 2^e for inv = 1 / l, reduced across
+// partial_exp: the exponent e with every |o| / 2^e below 1, reduced across
 // the row's lanes (every lane of the wave must call it).
 template <int D, int KV>
-__device__ __forceinline__ int partial_exp(const f32x4 (&o)[D / 16], float inv) {
+__device__ __forceinline__ int partial_exp(const f32x4 (&o)[D / 16]) {
   int e = 0;
   if constexpr (KV != kKvF32) {
     float amax = 0.f;
@@ -144,7 +145,6 @@ __device__ __forceinline__ int partial_exp(const f32x4 (&o)[D / 16], float inv) 
     for (int t = 0; t < D / 16; ++t)
 #pragma unroll
       for (int j = 0; j < 4; ++j) amax = fmaxf(amax, __builtin_fabsf(o[t][j]));
-    amax *= inv;
     amax = fmaxf(amax, __shfl_xor(amax, 16));
     amax = fmaxf(amax, __shfl_xor(amax, 32));
     // amax = f 2^e with f in [0.5, 1): every element over 2^e is in [-1, 1].
@@ -153,23 +153,27 @@ __device__ __forceinline__ int partial_exp(const f32x4 (&o)[D / 16], float inv) 
   return e;
 }
 
-// store_partial: the row's stores, with inv and e from above.
+// store_partial: the row's stores, with inv = 1 / l (0 for l = 0) and e
+// from above. (Scaling by 2^-e alone, not by 1 / l as well, takes one
+// instruction per element instead of two.)
 template <int D, int KV>
 __device__ __forceinline__ void store_partial(void* part_o, float* part_ml, int64_t prow, const f32x4 (&o)[D / 16],
                                               float m, float l, float inv, int e, int lq) {
+  float z = 1.f;
   if constexpr (KV != kKvF32) {
     uint32_t w[D / 8];
 #pragma unroll
     for (int t = 0; t < D / 16; ++t)
 #pragma unroll
       for (int j = 0; j < 4; j += 2) {
-        const f16x2 h = {static_cast<_Float16>(__builtin_ldexpf(o[t][j] * inv, -e)),
-                         static_cast<_Float16>(__builtin_ldexpf(o[t][j + 1] * inv, -e))};
+        const f16x2 h = {static_cast<_Float16>(__builtin_ldexpf(o[t][j], -e)),
+                         static_cast<_Float16>(__builtin_ldexpf(o[t][j + 1], -e))};
         w[2 * t + j / 2] = __builtin_bit_cast(uint32_t, h);
       }
     uint4* dst = reinterpret_cast<uint4*>(static_cast<uint16_t*>(part_o) + prow * D + (D / 4) * lq);
 #pragma unroll
     for (int c = 0; c < D / 32; ++c) dst[c] = uint4{w[4 * c], w[4 * c + 1], w[4 * c + 2], w[4 * c + 3]};
+    z = __builtin_ldexpf(inv, e);
   } else {
     f32x4* dst = reinterpret_cast<f32x4*>(static_cast<float*>(part_o) + prow * D + (D / 4) * lq);
 #pragma unroll
@@ -178,8 +182,7 @@ __device__ __forceinline__ void store_partial(void* part_o, float* part_ml, int6
   // A state without tokens (l = 0) takes no part in the merge's maximum; a
   // NaN m (a bad row) is kept.
   const float m_out = (l > 0.f || m != m) ? m : kNegInf;
-  if (lq == 0)
-    *reinterpret_cast<f32x4*>(part_ml + prow * kPartMl) = f32x4{m_out, l, __builtin_ldexpf(1.f, e), 0.f};
+  if (lq == 0) *reinterpret_cast<f32x4*>(part_ml + prow * kPartMl) = f32x4{m_out, l, z, 0.f};
 }
 
 // Both steps for one row; `active` says whether the row exists.
@@ -187,7 +190,7 @@ template <int D, int KV>
 __device__ __forceinline__ void write_partial(void* part_o, float* part_ml, int64_t prow, const f32x4 (&o)[D / 16],
                                               float m, float l, int lq, bool active) {
   const float inv = l > 0.f ? 1.f / l : 0.f;
-  const int e = partial_exp<D, KV>(o, inv);
+  const int e = partial_exp<D, KV>(o);
   if (active) store_partial<D, KV>(part_o, part_ml, prow, o, m, l, inv, e, lq);
 }
 
@@ -1025,7 +1028,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_kernel(AttnParams p) {
 #pragma unroll
         for (int i = 0; i < kWideTiles; ++i) inv_[i] = lw_[i] > 0.f ? 1.f / lw_[i] : 0.f;
 #pragma unroll
-        for (int i = 0; i < kWideTiles; ++i) e_[i] = partial_exp<D, KV>(st[i].o, inv_[i]);
+        for (int i = 0; i < kWideTiles; ++i) e_[i] = partial_exp<D, KV>(st[i].o);
 #pragma unroll
         for (int i = 0; i < kWideTiles; ++i) {
           if (wave + kWaves * i >= nt) continue;  // wave-uniform
@@ -1380,8 +1383,8 @@ struct MergeRaw<4, false> {
 // Exact merge of the partial softmax states of each (beam, query head), in
 // the order of the beam's slot list. With M = max_k m_k over the states
 // that saw tokens (l_k > 0), w_k = l_k 2^(m_k - M), and e_k the stored
-// elements o_k / (l_k s_k):
-//   out = sum_k w_k s_k e_k / sum_k w_k.
+// elements with factor z_k (e_k z_k = o_k / l_k):
+//   out = sum_k w_k z_k e_k / sum_k w_k.
 // A slot-table row of zeros for the paged path, which has no table (the
 // merges read their table entries without a branch).
 __device__ const int kZeroTabRow[kSlotTabReadAhead] = {};

@@ -68,16 +68,17 @@ struct UnitRec {
 static_assert(sizeof(UnitRec) == 32 + 4 * kMaxWideBeams + 16 * kMaxEntries, "UnitRec layout");
 
 // Partial softmax state of one query row over a subset of its tokens:
-// the reference maximum m (log2 units), the sum l of 2^(score - m), and
-// o / (l * s): the normalised value average divided by a power of two s,
-// the row's scale, chosen so that every element lies in [-1, 1]. The row
-// stores o / (l * s) in fp16 for bf16 and fp8 caches (2 bytes per element
-// instead of 4; with s the elements keep fp16's full relative precision
-// and never overflow) and in fp32 with s = 1 for fp32 caches. The D
+// the reference maximum m (log2 units), the sum l of 2^(score - m), the
+// row's elements and their factor z, with element x z = o / l (the
+// normalised value average). For bf16 and fp8 caches the elements are o
+// divided by a power of two 2^e chosen so that every element lies in
+// [-1, 1], in fp16 (2 bytes per element instead of 4; scaled so, the
+// elements keep fp16's full relative precision and never overflow), and
+// z = 2^e / l; for fp32 caches they are o / l in fp32 and z = 1. The D
 // elements of a row are stored in lane order: element 32 q + 4 t + j (for
 // D = 128; generally (D / 4) q + 4 t + j) holds dimension 16 t + 4 q + j,
 // the order in which the attention kernel's lanes hold the row.
-constexpr int kPartMl = 4;  // floats per row of part_ml: m, l, s, 0
+constexpr int kPartMl = 4;  // floats per row of part_ml: m, l, z, 0
 
 struct AttnParams {
   const void* q;
@@ -89,7 +90,7 @@ struct AttnParams {
   const int32_t* seq_lens;
   float* out;
   void* part_o;    // [rows][D] fp16 (fp32 for fp32 caches), lane order
-  float* part_ml;  // [rows][kPartMl]: m, l, s, 0
+  float* part_ml;  // [rows][kPartMl]: m, l, z, 0
   // prefix path (null recs: paged path)
   const UnitRec* recs;
   const int32_t* build_len;  // [S] lengths the metadata was built for
