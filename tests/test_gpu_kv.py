@@ -229,11 +229,12 @@ def test_beam_search_replay(kv):
             prev_meta = metas[0]
 
 
-@pytest.mark.parametrize("name", ["7b64", "7b_straggler"])
+@pytest.mark.parametrize("name", ["7b64", "7b_straggler", "7b64_balanced", "1p5b16"])
 def test_fork_prefix_meta_at_config_scale(name):
     """The metadata of the next search iteration re-planned warm from the current one's
     (tts_fork_prefix_meta: seed 1's tree after seed 0's, same shape): the same trie, segments and
-    beam order as a full build, and attention within tolerance of the oracle."""
+    beam order as a full build, and attention within tolerance of the oracle. (The balanced tree's plan has
+    128-row wide units and the 1.5B tree's 42-row narrow units, caps a warm re-plan keeps.)"""
     from oracle.attention import oracle_attn_workload
     from paper_2509_00195_amd.runner import PrefixAttention
     from tts_synth import make_workload
